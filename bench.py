@@ -1,0 +1,233 @@
+"""Benchmark of the Top-p block-sparse attention hot path on one MI355X.
+
+One step = fva_route (pool, scores, softmax, Top-p + floor, mask / counts /
+kept lists) + fva_attn (work list + block-sparse attention) over one batch of
+synthetic video-DiT inputs already resident in HBM. Default workload: the
+720p layer (40 heads, 21x45x80 latent tokens, 2x8x8 blocks, p = 0.9,
+k_min = 4), the shape the paper's attention numbers are quoted on.
+
+Prints ONE JSON line. `value` is dense-equivalent TFLOPS of the whole step:
+4 * heads * N^2 * d / step time (the dense attention work the step replaces).
+Beside it: attention ms, route us and route GB/s, kept-tile TFLOPS
+(4 * 128^2 * d per kept block pair), useful TFLOPS (real-token pairs), the
+retained fraction, a roofline object for the attention kernel and the fp64
+CPU oracle timed on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--workload 720p]
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sparse attn ms + dense-equiv TFLOPS, MFMA util on kept blocks; route GB/s"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBPS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def real_pairs(mask, geo):
+    """sum over kept (h, i, j) of n_i * n_j (real token pairs)."""
+    n = geo.block_sizes.astype(np.float64)
+    m = mask.reshape(-1, geo.nb, geo.nb).astype(np.float64)
+    return float(np.einsum("hij,i,j->", m, n, n))
+
+
+def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, geo, budget_s=20.0):
+    """Oracle timed on this host on a bounded sample; returns dict."""
+    from oracle import attn_ref_rows, route_ref
+
+    import synth
+
+    cores = len(os.sched_getaffinity(0))
+    f64 = lambda b: synth.bf16_bits_to_f32(b).astype(np.float64)
+    H = cfg.heads
+    # routing: a subset of heads, extrapolated linearly in heads
+    rh = list(range(0, H, max(1, H // 8)))
+    Qr, Kr = f64(Qb[0, rh]), f64(Kb[0, rh])
+    t0 = time.perf_counter()
+    route_ref(Qr, Kr, cfg.p, cfg.k_min, geo)
+    t_route = (time.perf_counter() - t0) * H / len(rh)
+    # attention: query blocks of the lowest- and highest-density heads and two
+    # others, until the time budget is used; extrapolated by real token pairs
+    dens = counts[0].mean(axis=-1)
+    heads = [int(np.argmin(dens)), int(np.argmax(dens)), H // 3, (2 * H) // 3]
+    n = geo.block_sizes.astype(np.float64)
+    heads_f64 = {h: (f64(Qb[0, h]), f64(Kb[0, h]), f64(Vb[0, h])) for h in heads}
+    rng = np.random.default_rng(7)
+    done_pairs = 0.0
+    t_att = 0.0
+    rows = 0
+    while t_att < budget_s:
+        for h in heads:
+            i = int(rng.integers(geo.nb))
+            t0 = time.perf_counter()
+            attn_ref_rows(*heads_f64[h], mask[0, h], geo, [i])
+            t_att += time.perf_counter() - t0
+            done_pairs += n[i] * float((mask[0, h, i].astype(np.float64) * n).sum())
+            rows += 1
+    total_pairs = real_pairs(mask, geo)
+    t_att_full = t_att * total_pairs / max(done_pairs, 1.0)
+    t_full = t_route + t_att_full
+    dense_flops = 4.0 * H * float(geo.N) ** 2 * 128
+    return {
+        "value": dense_flops / t_full / 1e12,
+        "unit": "TFLOPS (dense-equivalent)",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": f"fp64 numpy oracle: routing on {len(rh)} of {H} heads (scaled by heads), attention on "
+        f"{rows} query blocks of heads {heads} (scaled by real kept token pairs); extrapolated step "
+        f"{t_full:.1f} s (route {t_route:.1f} s + attention {t_att_full:.1f} s)",
+        "seconds_extrapolated": t_full,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="720p")
+    ap.add_argument("--p", type=float, default=None)
+    ap.add_argument("--sched", choices=["persistent", "naive"], default="persistent")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(
+            "bench.py measures one GPU only: the path shards by head across GPUs (see the design notes); "
+            "run with --gpus 1",
+            file=sys.stderr,
+        )
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_16190_amd as fva
+    import synth
+    from oracle.tiling import tile_geometry  # geometry tables for the work counts only
+
+    cfg = synth.get_config(args.workload)
+    p = cfg.p if args.p is None else args.p
+    geo = tile_geometry(*cfg.grid, *cfg.tile)
+    tiling = fva.Tiling(*cfg.grid, *cfg.tile)
+    dev = torch.device("cuda:0")
+    log(f"[bench] generating {cfg.name}: {cfg.heads} heads x {cfg.N} tokens x 128")
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    up = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+    q, k, v = up(Qb), up(Kb), up(Vb)
+    desc = fva._desc_of(q)
+    nb = geo.nb
+    B, H = q.shape[0], q.shape[1]
+    mask = torch.empty((B, H, nb, nb), dtype=torch.uint8, device=dev)
+    counts = torch.empty((B, H, nb), dtype=torch.int32, device=dev)
+    kv = torch.empty((B, H, nb, nb), dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    ws_r = torch.empty(fva.fva_route_workspace_size(desc, tiling), dtype=torch.uint8, device=dev)
+    ws_a = torch.empty(fva.fva_attn_workspace_size(desc, tiling), dtype=torch.uint8, device=dev)
+    flags = fva.FVA_SCHED_NAIVE if args.sched == "naive" else fva.FVA_SCHED_PERSISTENT
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        fva.fva_route(q, k, p, cfg.k_min, tiling, out=(mask, counts, kv), workspace=ws_r)
+        if ev:
+            ev[1].record(stream)
+        fva.fva_attn(q, k, v, tiling, mask, counts, kv, flags=flags, out=out, workspace=ws_a)
+        if ev:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps)")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    route_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    attn_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    ms_per_step = wall * 1e3 / args.steps
+    log(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step (route {np.mean(route_ms)*1e3:.1f} us, "
+        f"attn {np.mean(attn_ms):.3f} ms)")
+
+    m_np = mask.cpu().numpy()
+    c_np = counts.cpu().numpy()
+    kept = int(c_np.sum())
+    d = 128
+    N = cfg.N
+    t_attn = float(np.mean(attn_ms)) / 1e3
+    t_route = float(np.mean(route_ms)) / 1e3
+    kept_tile_flops = 4.0 * 128 * 128 * d * kept
+    useful_flops = 4.0 * d * real_pairs(m_np, geo)
+    dense_flops = 4.0 * B * H * float(N) ** 2 * d
+    route_bytes = 2.0 * B * H * N * d * 2 + B * H * nb * nb + 4.0 * B * H * nb + 4.0 * kept
+    res = {
+        "metric": METRIC,
+        "value": round(dense_flops / (ms_per_step / 1e3) / 1e12, 2),
+        "unit": "TFLOPS (dense-equivalent, route + attention step)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded video-shaped Q/K/V, sinusoidal (t,y,x) embedding, per-head alpha)",
+        "config": {
+            "workload": f"{cfg.name}: {H} heads, d=128, latent grid {'x'.join(map(str, cfg.grid))} = {N} tokens, "
+            f"tile {'x'.join(map(str, cfg.tile))}, nb={nb}, p={p}, k_min={cfg.k_min}",
+            "batch": B,
+            "heads": H,
+            "tokens": N,
+            "p": p,
+            "k_min": cfg.k_min,
+            "scheduler": args.sched,
+            "parallelism": "single GPU",
+        },
+        "attn_ms": round(t_attn * 1e3, 4),
+        "route_us": round(t_route * 1e6, 2),
+        "route_GBps": round(route_bytes / t_route / 1e9, 1),
+        "route_frac_hbm": round(route_bytes / t_route / 1e9 / PEAK_HBM_GBPS, 4),
+        "kept_tile_TFLOPS": round(kept_tile_flops / t_attn / 1e12, 2),
+        "kept_tile_frac_bf16_peak": round(kept_tile_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "useful_TFLOPS": round(useful_flops / t_attn / 1e12, 2),
+        "dense_equiv_attn_TFLOPS": round(dense_flops / t_attn / 1e12, 2),
+        "retained_fraction": round(kept / (B * H * nb * nb), 4),
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(useful_flops / t_attn / 1e12, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(useful_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+            "kernel": "attn_persistent_kernel (fva_attn; includes the one-workgroup plan kernel)",
+            "algorithmic_flops_per_launch": useful_flops,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        res["cpu_baseline"] = cpu_baseline(cfg, Qb, Kb, Vb, m_np, c_np, geo, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

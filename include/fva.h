@@ -1,0 +1,155 @@
+/*
+ * fva.h -- C ABI of the MI355X (gfx950) Top-p block-sparse video attention
+ * library (libfva.so).
+ *
+ * The library implements the per-step hot path of FVAttn's sparse attention
+ * ("Adaptive Sparse Attention with Runtime Load Balancing for Video
+ * Generation"): the routing frontend of §3.1 (video-aware 3D blocks,
+ * pooled block similarities, Top-p with a Top-k floor, §2.1) and
+ * block-sparse attention over the retained blocks (§2.1, §3.1).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Q, K, V, O are bf16 tensors of shape [batch, heads, tokens, head_dim]
+ *   with element strides (stride_b, stride_h, stride_n) and a contiguous
+ *   head_dim. All four use the strides of one fva_qkv_desc.
+ * - Tokens of a T x H x W latent grid are in raster order,
+ *   n = (t*H + y)*W + x. Blocks are bt x bh x bw boxes anchored at the
+ *   origin (a partial box only at the end of an axis); block ids are raster
+ *   order over the box grid; nb = ceil(T/bt)*ceil(H/bh)*ceil(W/bw). A block
+ *   holds only its real tokens (n_i <= bt*bh*bw); padding is never read.
+ * - Device pointers are device memory of the current HIP device; the
+ *   descriptor and tiling structs are host memory read during the call.
+ * - Ownership: the caller owns every buffer. The library keeps no state
+ *   between calls and allocates nothing; scratch space is the explicit
+ *   workspace, whose size the *_workspace_size queries return.
+ * - Asynchrony: every launching call is asynchronous on `stream` (a
+ *   hipStream_t; NULL is the default stream). It reads no device data on the
+ *   host and never synchronises; outputs are valid once the stream has
+ *   reached the call.
+ * - Errors: arguments are validated on the host before anything is
+ *   launched. On a negative status nothing was launched and no output was
+ *   written. FVA_ERR_HIP reports a failed kernel launch.
+ * - Reentrancy: calls may overlap on different streams if their workspaces
+ *   and outputs are distinct.
+ * - Supported shapes: head_dim == 128, bt*bh*bw in {64, 128}, nb <= 1024.
+ *   Anything else returns FVA_ERR_UNSUPPORTED (there is no slow generic path).
+ */
+#ifndef FVA_H
+#define FVA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum fva_status {
+  FVA_OK = 0,
+  FVA_ERR_INVALID_ARG = -1, /* null pointer, p outside [0,1] or NaN, k_min < 0, bad flags */
+  FVA_ERR_SHAPE = -2,       /* tokens != T*H*W, non-positive extents, bad strides */
+  FVA_ERR_UNSUPPORTED = -3, /* head_dim != 128, tile volume not 64/128, nb > 1024 */
+  FVA_ERR_WORKSPACE = -4,   /* workspace missing or smaller than the query says */
+  FVA_ERR_HIP = -5          /* a kernel launch failed */
+} fva_status;
+
+/* Latent grid (T x H x W) and 3D block box (bt x bh x bw). */
+typedef struct fva_tiling {
+  int32_t T, H, W;
+  int32_t bt, bh, bw;
+} fva_tiling;
+
+/* Shape and element strides of Q, K, V and O ([batch, heads, tokens, head_dim]). */
+typedef struct fva_qkv_desc {
+  int32_t batch, heads, tokens, head_dim;
+  int64_t stride_b, stride_h, stride_n; /* in elements; head_dim stride is 1 */
+} fva_qkv_desc;
+
+/* fva_attn flags. */
+#define FVA_SCHED_PERSISTENT 0u /* persistent grid pulling (head, query-block) items, heaviest first */
+#define FVA_SCHED_NAIVE 1u      /* one workgroup per item in head-major order (same kernel body) */
+#define FVA_TRACE 2u            /* record per-item start/end clock and CU id into `trace` */
+
+/* Number of blocks of a tiling, or -1 if an extent is not positive. Host only. */
+int32_t fva_num_blocks(const fva_tiling* tiling);
+
+/*
+ * Workspace bytes needed by fva_route for this shape: the pooled block means
+ * of Q and K in fp64, 2 * batch*heads*nb*128*8 bytes, 256-byte aligned.
+ */
+fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes);
+
+/*
+ * fva_route -- routing frontend (§3.1; Top-p and the Top-k floor of §2.1).
+ *
+ * For every (b, h) and query block i:
+ *   qbar_i, kbar_j = means of Q and K over the real tokens of each block;
+ *   s_ij = qbar_i . kbar_j / sqrt(128), P_ij = softmax over all j of s_ij;
+ *   key blocks ordered by decreasing s_ij (ties: lower j first), c_r the
+ *   running sum of their P; m_p = min{r : c_r >= p} (nb if none reaches p,
+ *   and nb when p == 1); m = max(m_p, min(k_min, nb)); the first m blocks of
+ *   that order are kept.
+ * All routing arithmetic is fp64. The running sums are exact fixed-point
+ * sums of the fp64 probabilities (2^-62 quanta), so the decision c_r >= p
+ * agrees with an fp64 sequential sum except within ~1e-15 of p.
+ *
+ * Inputs : Q, K (bf16, desc), p in [0, 1], k_min >= 0, tiling.
+ * Outputs: block_mask uint8 [batch, heads, nb, nb] (1 = kept), fully written;
+ *          counts int32 [batch, heads, nb] = m per row, fully written;
+ *          kv_idx int32 [batch, heads, nb, nb] or NULL: row (b,h,i) holds the
+ *          kept block ids in ascending order in its first counts[b,h,i]
+ *          entries; later entries are left untouched.
+ * workspace: at least fva_route_workspace_size bytes of device memory,
+ *          256-byte aligned.
+ */
+fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
+                     const fva_tiling* tiling, uint8_t* block_mask, int32_t* counts, int32_t* kv_idx,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Workspace bytes needed by fva_attn for this shape and flags: the work
+ * list and queue counters, plus room for counts and kv_idx (batch*heads*nb
+ * and batch*heads*nb*nb int32) used when the caller passes them as NULL.
+ */
+fva_status fva_attn_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, uint32_t flags,
+                                   size_t* bytes);
+
+/* Number of int64 words `trace` must hold under FVA_TRACE: 4 per (b, h, i) row. */
+int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling);
+
+/*
+ * fva_attn -- block-sparse attention over the retained blocks (§2.1: only
+ * the selected query-key block pairs are evaluated; §3.1).
+ *
+ * For every real query token n of block i of (b, h):
+ *   O_n = sum over the real tokens k of every key block j with
+ *         block_mask[b,h,i,j] = 1 of softmax_k(softmax_scale * Q_n . K_k) V_k,
+ * and O_n = 0 when the row keeps no block. bf16 MFMA products, fp32
+ * accumulation and softmax statistics, bf16 output.
+ *
+ * block_mask: uint8 [batch, heads, nb, nb], any 0/1 pattern.
+ * counts, kv_idx: either both NULL (they are rebuilt from block_mask in the
+ *          workspace) or both given in the layout fva_route writes, and then
+ *          they must describe block_mask exactly.
+ * softmax_scale: <= 0 selects 1/sqrt(128).
+ * flags: FVA_SCHED_PERSISTENT or FVA_SCHED_NAIVE, optionally | FVA_TRACE.
+ * O: bf16, same strides as Q; every real token row is written.
+ * trace: device int64 [fva_trace_words] when FVA_TRACE is set, else ignored.
+ *        Row r = (b*heads + h)*nb + i gets {start clock, end clock,
+ *        (xcc_id << 16) | hw_id low bits, workgroup id}; clocks are the
+ *        100 MHz constant device clock.
+ */
+fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_desc* desc,
+                    const fva_tiling* tiling, const uint8_t* block_mask, const int32_t* counts,
+                    const int32_t* kv_idx, float softmax_scale, uint32_t flags, void* O, void* workspace,
+                    size_t workspace_bytes, void* trace, void* stream);
+
+/* Static description of a status code. */
+const char* fva_status_string(fva_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FVA_H */

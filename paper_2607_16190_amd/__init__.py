@@ -1,0 +1,233 @@
+"""Python binding of libfva.so: Top-p block-sparse video attention on MI355X.
+
+Argument marshalling only: every step of the path runs in the gfx950 kernels
+behind the C ABI declared in include/fva.h. PyTorch supplies device memory
+and the current stream. Importing this module fails loudly when the library
+has not been built; there is no fallback implementation.
+
+    import paper_2607_16190_amd as fva
+    mask, counts, kv_idx = fva.fva_route(q, k, 0.9, 4, fva.Tiling(21, 45, 80, 2, 8, 8))
+    out = fva.fva_attn(q, k, v, tiling, mask, counts, kv_idx)
+"""
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfva.so")
+
+FVA_OK = 0
+FVA_ERR_INVALID_ARG = -1
+FVA_ERR_SHAPE = -2
+FVA_ERR_UNSUPPORTED = -3
+FVA_ERR_WORKSPACE = -4
+FVA_ERR_HIP = -5
+
+FVA_SCHED_PERSISTENT = 0
+FVA_SCHED_NAIVE = 1
+FVA_TRACE = 2
+
+EXPORTED = (
+    "fva_num_blocks",
+    "fva_route_workspace_size",
+    "fva_route",
+    "fva_attn_workspace_size",
+    "fva_trace_words",
+    "fva_attn",
+    "fva_status_string",
+)
+
+
+class _Tiling(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("T", "H", "W", "bt", "bh", "bw")]
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("heads", ctypes.c_int32),
+        ("tokens", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("stride_b", ctypes.c_int64),
+        ("stride_h", ctypes.c_int64),
+        ("stride_n", ctypes.c_int64),
+    ]
+
+
+@dataclass(frozen=True)
+class Tiling:
+    """T x H x W latent grid cut into bt x bh x bw blocks."""
+
+    T: int
+    H: int
+    W: int
+    bt: int
+    bh: int
+    bw: int
+
+    def c(self) -> _Tiling:
+        return _Tiling(self.T, self.H, self.W, self.bt, self.bh, self.bw)
+
+    @property
+    def tokens(self) -> int:
+        return self.T * self.H * self.W
+
+
+class FvaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {fva_status_string(status)} (status {status})")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build the HIP library first "
+            "(python -c 'import __graft_entry__ as g; g.build()')"
+        )
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    T = ctypes.POINTER(_Tiling)
+    D = ctypes.POINTER(_Desc)
+    sz = ctypes.POINTER(ctypes.c_size_t)
+    sigs = {
+        "fva_num_blocks": (ctypes.c_int32, [T]),
+        "fva_route_workspace_size": (ctypes.c_int, [D, T, sz]),
+        "fva_route": (
+            ctypes.c_int,
+            [P, P, D, ctypes.c_double, ctypes.c_int32, T, P, P, P, P, ctypes.c_size_t, P],
+        ),
+        "fva_attn_workspace_size": (ctypes.c_int, [D, T, ctypes.c_uint32, sz]),
+        "fva_trace_words": (ctypes.c_int64, [D, T]),
+        "fva_attn": (
+            ctypes.c_int,
+            [P, P, P, D, T, P, P, P, ctypes.c_float, ctypes.c_uint32, P, P, ctypes.c_size_t, P, P],
+        ),
+        "fva_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+
+
+def fva_status_string(status: int) -> str:
+    return lib.fva_status_string(int(status)).decode()
+
+
+def fva_num_blocks(tiling: Tiling) -> int:
+    return int(lib.fva_num_blocks(ctypes.byref(tiling.c())))
+
+
+def _desc_of(x) -> _Desc:
+    if x.dim() != 4:
+        raise ValueError("expected a [batch, heads, tokens, head_dim] tensor")
+    if x.stride(3) != 1:
+        raise ValueError("head_dim must be contiguous")
+    B, H, N, D = x.shape
+    return _Desc(B, H, N, D, x.stride(0), x.stride(1), x.stride(2))
+
+
+def _check(status: int, where: str):
+    if status != FVA_OK:
+        raise FvaError(status, where)
+
+
+def fva_route_workspace_size(desc: _Desc, tiling: Tiling) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.fva_route_workspace_size(ctypes.byref(desc), ctypes.byref(tiling.c()), ctypes.byref(n)), "fva_route_workspace_size")
+    return n.value
+
+
+def fva_attn_workspace_size(desc: _Desc, tiling: Tiling, flags: int = 0) -> int:
+    n = ctypes.c_size_t(0)
+    _check(
+        lib.fva_attn_workspace_size(ctypes.byref(desc), ctypes.byref(tiling.c()), int(flags), ctypes.byref(n)),
+        "fva_attn_workspace_size",
+    )
+    return n.value
+
+
+def fva_trace_words(desc: _Desc, tiling: Tiling) -> int:
+    return int(lib.fva_trace_words(ctypes.byref(desc), ctypes.byref(tiling.c())))
+
+
+def _stream_ptr(torch, stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _workspace(torch, nbytes: int, device, workspace):
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError("workspace too small")
+        return workspace
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def fva_route(q, k, p: float, k_min: int, tiling: Tiling, *, kv_idx: bool = True, out=None, workspace=None, stream=None):
+    """Top-p block routing (see include/fva.h). Returns (mask, counts, kv_idx or None)."""
+    import torch
+
+    if q.dtype != torch.bfloat16 or k.dtype != torch.bfloat16 or not q.is_cuda or not k.is_cuda:
+        raise ValueError("q and k must be bf16 device tensors")
+    if q.shape != k.shape or q.stride() != k.stride():
+        raise ValueError("q and k must share shape and strides")
+    desc = _desc_of(q)
+    nb = fva_num_blocks(tiling)
+    B, H = q.shape[0], q.shape[1]
+    if out is None:
+        mask = torch.empty((B, H, max(nb, 0), max(nb, 0)), dtype=torch.uint8, device=q.device)
+        counts = torch.empty((B, H, max(nb, 0)), dtype=torch.int32, device=q.device)
+        kv = torch.empty((B, H, max(nb, 0), max(nb, 0)), dtype=torch.int32, device=q.device) if kv_idx else None
+    else:
+        mask, counts, kv = out
+    ws = _workspace(torch, fva_route_workspace_size(desc, tiling), q.device, workspace)
+    st = lib.fva_route(
+        _ptr(q), _ptr(k), ctypes.byref(desc), float(p), int(k_min), ctypes.byref(tiling.c()),
+        _ptr(mask), _ptr(counts), _ptr(kv), _ptr(ws), ctypes.c_size_t(ws.numel() * ws.element_size()),
+        _stream_ptr(torch, stream),
+    )
+    _check(st, "fva_route")
+    return mask, counts, kv
+
+
+def fva_attn(q, k, v, tiling: Tiling, mask, counts=None, kv_idx=None, *, scale: float = 0.0, flags: int = 0,
+             out=None, workspace=None, trace=None, stream=None):
+    """Block-sparse attention over the kept blocks (see include/fva.h). Returns O."""
+    import torch
+
+    for t in (q, k, v):
+        if t.dtype != torch.bfloat16 or not t.is_cuda:
+            raise ValueError("q, k, v must be bf16 device tensors")
+    if not (q.shape == k.shape == v.shape) or not (q.stride() == k.stride() == v.stride()):
+        raise ValueError("q, k, v must share shape and strides")
+    desc = _desc_of(q)
+    if out is None:
+        out = torch.empty_strided(q.shape, q.stride(), dtype=torch.bfloat16, device=q.device)
+    elif out.stride() != q.stride() or out.shape != q.shape or out.dtype != torch.bfloat16:
+        raise ValueError("out must match q in shape, strides and dtype")
+    ws = _workspace(torch, fva_attn_workspace_size(desc, tiling, flags & 3), q.device, workspace)
+    if (flags & FVA_TRACE) and trace is None:
+        raise ValueError("FVA_TRACE needs a trace tensor of fva_trace_words int64")
+    st = lib.fva_attn(
+        _ptr(q), _ptr(k), _ptr(v), ctypes.byref(desc), ctypes.byref(tiling.c()), _ptr(mask), _ptr(counts),
+        _ptr(kv_idx), ctypes.c_float(scale), int(flags), _ptr(out), _ptr(ws),
+        ctypes.c_size_t(ws.numel() * ws.element_size()), _ptr(trace), _stream_ptr(torch, stream),
+    )
+    _check(st, "fva_attn")
+    return out
+
+
+def default_scale(head_dim: int = 128) -> float:
+    return 1.0 / math.sqrt(head_dim)

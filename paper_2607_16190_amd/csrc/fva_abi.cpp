@@ -1,0 +1,166 @@
+// C ABI of libfva.so: argument validation, workspace sizing and launch
+// sequencing. Every check runs on the host before anything is launched.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/fva.h"
+#include "fva_geometry.h"
+#include "fva_internal.h"
+
+namespace {
+
+bool tiling_ok(const fva_tiling* t) {
+  return t && t->T > 0 && t->H > 0 && t->W > 0 && t->bt > 0 && t->bh > 0 && t->bw > 0;
+}
+
+// Shape checks shared by route and attn; returns FVA_OK or the error.
+fva_status check_shape(const fva_qkv_desc* d, const fva_tiling* t, int* nb_out) {
+  if (!d || !t) return FVA_ERR_INVALID_ARG;
+  if (!tiling_ok(t)) return FVA_ERR_SHAPE;
+  if (d->batch < 0 || d->heads < 0 || d->tokens <= 0) return FVA_ERR_SHAPE;
+  const int64_t n = (int64_t)t->T * t->H * t->W;
+  if (n != (int64_t)d->tokens) return FVA_ERR_SHAPE;
+  if (d->head_dim != fva::kHeadDim) return FVA_ERR_UNSUPPORTED;
+  const int64_t vol = (int64_t)t->bt * t->bh * t->bw;
+  if (vol != 64 && vol != 128) return FVA_ERR_UNSUPPORTED;
+  const fva::Geometry g = fva::make_geometry(t->T, t->H, t->W, t->bt, t->bh, t->bw);
+  if (g.nb > fva::kMaxBlocks) return FVA_ERR_UNSUPPORTED;
+  // Strides are in elements; every token row must start on a 16-byte boundary.
+  if (d->stride_n < d->head_dim || d->stride_h < 0 || d->stride_b < 0) return FVA_ERR_SHAPE;
+  if (d->stride_n % 8 != 0 || d->stride_h % 8 != 0 || d->stride_b % 8 != 0) return FVA_ERR_SHAPE;
+  *nb_out = g.nb;
+  return FVA_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t fva_num_blocks(const fva_tiling* tiling) {
+  if (!tiling_ok(tiling)) return -1;
+  const int64_t nb = (int64_t)((tiling->T + tiling->bt - 1) / tiling->bt) * ((tiling->H + tiling->bh - 1) / tiling->bh) *
+                     ((tiling->W + tiling->bw - 1) / tiling->bw);
+  return nb > INT32_MAX ? -1 : (int32_t)nb;
+}
+
+fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes) {
+  if (!bytes) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  *bytes = fva::route_workspace_bytes(desc->batch, desc->heads, nb);
+  return FVA_OK;
+}
+
+fva_status fva_attn_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, uint32_t flags, size_t* bytes) {
+  if (!bytes) return FVA_ERR_INVALID_ARG;
+  if (flags & ~3u) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  *bytes = fva::attn_workspace_bytes(desc->batch, desc->heads, nb);
+  return FVA_OK;
+}
+
+int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling) {
+  int nb = 0;
+  if (check_shape(desc, tiling, &nb) != FVA_OK) return -1;
+  return (int64_t)desc->batch * desc->heads * nb * 4;
+}
+
+fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
+                     const fva_tiling* tiling, uint8_t* block_mask, int32_t* counts, int32_t* kv_idx, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (!Q || !K || !block_mask || !counts) return FVA_ERR_INVALID_ARG;
+  if (std::isnan(p) || p < 0.0 || p > 1.0 || k_min < 0) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  if (!aligned16(Q) || !aligned16(K)) return FVA_ERR_INVALID_ARG;
+  const size_t need = fva::route_workspace_bytes(desc->batch, desc->heads, nb);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;
+  fva::RouteArgs a;
+  a.Q = Q;
+  a.K = K;
+  a.batch = desc->batch;
+  a.heads = desc->heads;
+  a.tokens = desc->tokens;
+  a.stride_b = desc->stride_b;
+  a.stride_h = desc->stride_h;
+  a.stride_n = desc->stride_n;
+  a.T = tiling->T;
+  a.H = tiling->H;
+  a.W = tiling->W;
+  a.bt = tiling->bt;
+  a.bh = tiling->bh;
+  a.bw = tiling->bw;
+  a.p = p;
+  a.k_min = k_min;
+  a.mask = block_mask;
+  a.counts = counts;
+  a.kv_idx = kv_idx;
+  a.workspace = workspace;
+  a.stream = reinterpret_cast<hipStream_t>(stream);
+  return fva::launch_route(a) == hipSuccess ? FVA_OK : FVA_ERR_HIP;
+}
+
+fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_desc* desc, const fva_tiling* tiling,
+                    const uint8_t* block_mask, const int32_t* counts, const int32_t* kv_idx, float softmax_scale,
+                    uint32_t flags, void* O, void* workspace, size_t workspace_bytes, void* trace, void* stream) {
+  if (!Q || !K || !V || !O) return FVA_ERR_INVALID_ARG;
+  if (flags & ~3u) return FVA_ERR_INVALID_ARG;
+  if ((counts == nullptr) != (kv_idx == nullptr)) return FVA_ERR_INVALID_ARG;
+  if (!counts && !block_mask) return FVA_ERR_INVALID_ARG;
+  if ((flags & FVA_TRACE) && !trace) return FVA_ERR_INVALID_ARG;
+  if (std::isnan(softmax_scale) || std::isinf(softmax_scale)) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return FVA_ERR_INVALID_ARG;
+  const size_t need = fva::attn_workspace_bytes(desc->batch, desc->heads, nb);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;
+  fva::AttnArgs a;
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.O = O;
+  a.batch = desc->batch;
+  a.heads = desc->heads;
+  a.tokens = desc->tokens;
+  a.stride_b = desc->stride_b;
+  a.stride_h = desc->stride_h;
+  a.stride_n = desc->stride_n;
+  a.T = tiling->T;
+  a.H = tiling->H;
+  a.W = tiling->W;
+  a.bt = tiling->bt;
+  a.bh = tiling->bh;
+  a.bw = tiling->bw;
+  a.mask = block_mask;
+  a.counts = counts;
+  a.kv_idx = kv_idx;
+  a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt(128.0f);
+  a.flags = flags;
+  a.trace = reinterpret_cast<int64_t*>(trace);
+  a.workspace = workspace;
+  a.stream = reinterpret_cast<hipStream_t>(stream);
+  return fva::launch_attn(a) == hipSuccess ? FVA_OK : FVA_ERR_HIP;
+}
+
+const char* fva_status_string(fva_status status) {
+  switch (status) {
+    case FVA_OK: return "ok";
+    case FVA_ERR_INVALID_ARG: return "invalid argument";
+    case FVA_ERR_SHAPE: return "shape mismatch";
+    case FVA_ERR_UNSUPPORTED: return "unsupported shape (head_dim must be 128, tile volume 64 or 128, nb <= 1024)";
+    case FVA_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case FVA_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,49 @@
+// Internal launch interface between the C ABI layer and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fva {
+
+struct RouteArgs {
+  const void* Q;
+  const void* K;
+  int batch, heads, tokens;
+  int64_t stride_b, stride_h, stride_n;
+  int T, H, W, bt, bh, bw;
+  double p;
+  int k_min;
+  uint8_t* mask;
+  int32_t* counts;
+  int32_t* kv_idx;  // may be null
+  void* workspace;
+  hipStream_t stream;
+};
+
+struct AttnArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  void* O;
+  int batch, heads, tokens;
+  int64_t stride_b, stride_h, stride_n;
+  int T, H, W, bt, bh, bw;
+  const uint8_t* mask;
+  const int32_t* counts;  // null: rebuilt from mask in the workspace
+  const int32_t* kv_idx;  // null together with counts
+  float scale;
+  uint32_t flags;
+  int64_t* trace;  // null unless tracing
+  void* workspace;
+  hipStream_t stream;
+};
+
+size_t route_workspace_bytes(int batch, int heads, int nb);
+size_t attn_workspace_bytes(int batch, int heads, int nb);
+
+hipError_t launch_route(const RouteArgs& a);
+hipError_t launch_attn(const AttnArgs& a);
+
+}  // namespace fva

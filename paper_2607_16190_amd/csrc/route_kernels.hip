@@ -1,0 +1,415 @@
+// Routing frontend on gfx950: block pooling and Top-p / Top-k selection.
+//
+// pool_kernel   -- qbar_i, kbar_i = fp64 means of Q, K over the real tokens
+//                  of block i (pooled block similarities, §3.1). One workgroup
+//                  per (b, h, i) streams the block's rows of Q and K once;
+//                  sixteen lanes cover one 256-byte token row, so every wave
+//                  load is a run of whole rows.
+// select_kernel -- for 16 query blocks of one (b, h): fp64 scores against
+//                  every key block, softmax, Top-p cut with the Top-k floor
+//                  (§2.1), then the mask row, the count and the ascending
+//                  kept-block list. One wavefront owns one row at a time.
+//
+// The Top-p cut never sorts the row. The probabilities are turned into exact
+// fixed-point masses F_j = round(P_j * 2^62), so every partial sum is exact
+// and order-free; a bucketed radix select over the scores (64 buckets per
+// level, ordered from the highest score) finds the bucket in which the
+// running mass first reaches T = ceil(p * 2^62), then recurses into that
+// bucket until at most 64 candidates remain, which are ranked exactly by
+// (score desc, block id asc). The result equals the sequential-sum definition
+// except where a running sum lies within a few 2^-62 quanta (plus the fp64
+// rounding of P) of p.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fva_common.h"
+#include "fva_geometry.h"
+#include "fva_internal.h"
+
+namespace fva {
+
+namespace {
+
+constexpr int kPoolThreads = 256;
+constexpr int kSelRows = 16;         // query blocks per select workgroup
+constexpr double kMassScale = 4611686018427387904.0;  // 2^62
+
+__global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __restrict__ Q,
+                                                           const uint16_t* __restrict__ K, int heads,
+                                                           int64_t sb, int64_t sh, int64_t sn, Geometry g,
+                                                           double* __restrict__ qbar,
+                                                           double* __restrict__ kbar) {
+  __shared__ double red[2][16][kHeadDim];
+  const int i = blockIdx.x;
+  const int bh = blockIdx.y;
+  const int b = bh / heads;
+  const int h = bh - b * heads;
+  const int64_t base = (int64_t)b * sb + (int64_t)h * sh;
+  const BlockBox box = block_box(g, i);
+  const int c = threadIdx.x & 15;    // 16-byte chunk: dims 8c .. 8c+7
+  const int slot = threadIdx.x >> 4;  // token slot 0..15
+
+  uint4 vq[8], vk[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int r = slot + 16 * u;
+    if (r < box.n) {
+      const int64_t off = base + (int64_t)box_token(g, box, r) * sn + c * 8;
+      vq[u] = *reinterpret_cast<const uint4*>(Q + off);
+      vk[u] = *reinterpret_cast<const uint4*>(K + off);
+    } else {
+      vq[u] = make_uint4(0, 0, 0, 0);
+      vk[u] = make_uint4(0, 0, 0, 0);
+    }
+  }
+  double aq[8], ak[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) { aq[e] = 0.0; ak[e] = 0.0; }
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const uint32_t wq[4] = {vq[u].x, vq[u].y, vq[u].z, vq[u].w};
+    const uint32_t wk[4] = {vk[u].x, vk[u].y, vk[u].z, vk[u].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      aq[2 * e] += (double)bf16_lo(wq[e]);
+      aq[2 * e + 1] += (double)bf16_hi(wq[e]);
+      ak[2 * e] += (double)bf16_lo(wk[e]);
+      ak[2 * e + 1] += (double)bf16_hi(wk[e]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    red[0][slot][c * 8 + e] = aq[e];
+    red[1][slot][c * 8 + e] = ak[e];
+  }
+  __syncthreads();
+  const int which = threadIdx.x >> 7;  // 0: Q, 1: K
+  const int d = threadIdx.x & 127;
+  double s = 0.0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) s += red[which][k][d];
+  double* out = which ? kbar : qbar;
+  out[((int64_t)bh * g.nb + i) * kHeadDim + d] = s / (double)box.n;
+}
+
+// Fixed-point mass of one block: round(exp(s - smax) / Z * 2^62).
+__device__ __forceinline__ uint64_t block_mass(double s, double smax, double Z) {
+  const double P = __ddiv_rn(exp(s - smax), Z);
+  return (uint64_t)__double2ull_rn(__dmul_rn(P, kMassScale));
+}
+
+struct WaveScratch {
+  uint32_t cnt[64];
+  uint64_t wt[64];
+  int list_j[64];
+  int slot_j[64];
+  uint64_t slot_w[64];
+};
+
+struct Cut {
+  double s;
+  int j;
+  int rank;  // 1-based position of the cut block in (score desc, id asc) order
+};
+
+// Finds the block q at which the running weight (fixed-point mass, or 1 per
+// block when by_mass is false) first reaches thr, walking blocks in
+// (score desc, id asc) order. Requires thr >= 1 and total weight >= thr.
+template <int KPL>
+__device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL], const uint64_t (&F)[KPL],
+                          uint32_t valid, double smin, double smax, double Z, bool by_mass, uint64_t thr,
+                          WaveScratch& ws, int lane) {
+  uint32_t cand = valid;
+  uint64_t W0 = 0;
+  int C0 = 0;
+  double lo = smin, hi = smax;
+  for (int level = 0; level < 2 * kMaxBlocks; ++level) {  // each level drops >= 1 candidate
+    int ncand = 0;
+#pragma unroll
+    for (int k = 0; k < KPL; ++k) ncand += __popcll(__ballot((cand >> k) & 1u));
+    if (ncand <= 64 || !(hi > lo)) {
+      // Gather the candidates in ascending block id order.
+      int base = 0;
+#pragma unroll
+      for (int k = 0; k < KPL; ++k) {
+        const bool is = (cand >> k) & 1u;
+        const uint64_t m = __ballot(is);
+        if (is) {
+          const int pos = base + lanes_below(m);
+          if (pos < 64) ws.list_j[pos] = lane + 64 * k;
+        }
+        base += __popcll(m);
+      }
+      wave_sync();
+      if (!(hi > lo) && ncand > 64) {
+        // Every candidate has the same score: they follow in id order, each
+        // with the same weight, so the cut is the t-th smallest id.
+        const uint64_t w = by_mass ? block_mass(hi, smax, Z) : 1ull;
+        const uint64_t need = thr - W0;
+        uint64_t t = (w == 0) ? (uint64_t)ncand : (need + w - 1) / w;
+        if (t > (uint64_t)ncand) t = (uint64_t)ncand;
+        if (t < 1) t = 1;
+        int seen = 0;
+        int cut_j = -1;
+#pragma unroll
+        for (int k = 0; k < KPL; ++k) {
+          const bool is = (cand >> k) & 1u;
+          const uint64_t m = __ballot(is);
+          const int cntk = __popcll(m);
+          if (cut_j < 0 && seen + cntk >= (int)t) {
+            const int want = (int)t - seen;  // 1-based within this k
+            if (is && lanes_below(m) + 1 == want) ws.list_j[0] = lane + 64 * k;
+            wave_sync();
+            cut_j = ws.list_j[0];
+          }
+          seen += cntk;
+        }
+        Cut c;
+        c.j = cut_j;
+        c.s = srow[cut_j];
+        c.rank = C0 + (int)t;
+        return c;
+      }
+      // At most 64 candidates: rank them exactly.
+      const bool has = lane < ncand;
+      const int jl = has ? ws.list_j[lane] : 0;
+      double sl = srow[jl];
+      int rank = 0;
+      for (int m = 0; m < ncand; ++m) {  // ncand <= 64 here
+        const int jm = ws.list_j[m];
+        const double sm = srow[jm];
+        rank += (sm > sl || (sm == sl && jm < jl)) ? 1 : 0;
+      }
+      const uint64_t wl = has ? (by_mass ? block_mass(sl, smax, Z) : 1ull) : 0ull;
+      wave_sync();
+      if (has && rank < 64) {
+        ws.slot_j[rank] = jl;
+        ws.slot_w[rank] = wl;
+      }
+      wave_sync();
+      const uint64_t myw = has ? ws.slot_w[lane] : 0ull;
+      const uint64_t cum = W0 + wave_incl_scan_u64(myw, lane);
+      const uint64_t hit = __ballot(has && cum >= thr);
+      int pos = hit ? (__ffsll((unsigned long long)hit) - 1) : (ncand - 1);
+      Cut c;
+      c.j = ws.slot_j[pos];
+      c.s = srow[c.j];
+      c.rank = C0 + pos + 1;
+      wave_sync();
+      return c;
+    }
+    // Bucket the candidates by score, highest scores in bucket 0.
+    ws.cnt[lane] = 0u;
+    ws.wt[lane] = 0ull;
+    wave_sync();
+    const double span = hi - lo;
+#pragma unroll
+    for (int k = 0; k < KPL; ++k) {
+      if ((cand >> k) & 1u) {
+        int bkt = (int)(64.0 * __ddiv_rn(hi - s[k], span));
+        bkt = bkt < 0 ? 0 : (bkt > 63 ? 63 : bkt);
+        atomicAdd(&ws.cnt[bkt], 1u);
+        atomicAdd((unsigned long long*)&ws.wt[bkt], (unsigned long long)(by_mass ? F[k] : 1ull));
+      }
+    }
+    wave_sync();
+    const uint64_t wb = ws.wt[lane];
+    const int cb = (int)ws.cnt[lane];
+    const uint64_t cumw = W0 + wave_incl_scan_u64(wb, lane);
+    const int cumc = wave_incl_scan_i32(cb, lane);
+    const uint64_t hit = __ballot(cumw >= thr);
+    const int bstar = hit ? (__ffsll((unsigned long long)hit) - 1) : 63;
+    W0 = __shfl(cumw - wb, bstar);
+    C0 += __shfl(cumc - cb, bstar);
+    wave_sync();
+    double nlo = 1.0e308, nhi = -1.0e308;
+#pragma unroll
+    for (int k = 0; k < KPL; ++k) {
+      if ((cand >> k) & 1u) {
+        int bkt = (int)(64.0 * __ddiv_rn(hi - s[k], span));
+        bkt = bkt < 0 ? 0 : (bkt > 63 ? 63 : bkt);
+        if (bkt != bstar) {
+          cand &= ~(1u << k);
+        } else {
+          nlo = fmin(nlo, s[k]);
+          nhi = fmax(nhi, s[k]);
+        }
+      }
+    }
+    lo = wave_min(nlo);
+    hi = wave_max(nhi);
+  }
+  // Not reached for finite scores; keep every block as a safe fallback.
+  Cut c;
+  c.j = -1;
+  c.s = -1.0e308;
+  c.rank = 0;
+  return c;
+}
+
+template <int KPL>
+__device__ void select_row(const double* __restrict__ srow, int nb, double p, int k_min, uint8_t* __restrict__ mrow,
+                           int32_t* __restrict__ count_out, int32_t* __restrict__ kvrow, WaveScratch& ws,
+                           int lane) {
+  double s[KPL];
+  uint64_t F[KPL];
+  uint32_t valid = 0;
+  double vmax = -1.0e308, vmin = 1.0e308;
+#pragma unroll
+  for (int k = 0; k < KPL; ++k) {
+    const int j = lane + 64 * k;
+    if (j < nb) {
+      s[k] = srow[j];
+      valid |= 1u << k;
+      vmax = fmax(vmax, s[k]);
+      vmin = fmin(vmin, s[k]);
+    } else {
+      s[k] = -1.0e308;
+    }
+  }
+  const double smax = wave_max(vmax);
+  const double smin = wave_min(vmin);
+  double e = 0.0;
+#pragma unroll
+  for (int k = 0; k < KPL; ++k)
+    if ((valid >> k) & 1u) e += exp(s[k] - smax);
+  const double Z = wave_sum(e);
+  uint64_t tot = 0;
+#pragma unroll
+  for (int k = 0; k < KPL; ++k) {
+    F[k] = ((valid >> k) & 1u) ? block_mass(s[k], smax, Z) : 0ull;
+    tot += F[k];
+  }
+  const uint64_t total = wave_sum_u64(tot);
+
+  const int kf = k_min < nb ? k_min : nb;
+  int m_p;
+  Cut cut;
+  cut.j = -1;
+  cut.s = 0.0;
+  cut.rank = 0;
+  if (p >= 1.0) {
+    m_p = nb;
+  } else {
+    const uint64_t T = (uint64_t)ceil(p * kMassScale);
+    if (T == 0) {
+      m_p = 0;
+    } else if (total < T) {
+      m_p = nb;
+    } else {
+      cut = select_cut<KPL>(srow, s, F, valid, smin, smax, Z, true, T, ws, lane);
+      m_p = cut.rank;
+    }
+  }
+  const int m = m_p > kf ? m_p : kf;
+  if (m > 0 && m < nb && m != m_p) cut = select_cut<KPL>(srow, s, F, valid, smin, smax, Z, false, (uint64_t)m, ws, lane);
+
+  int base = 0;
+#pragma unroll
+  for (int k = 0; k < KPL; ++k) {
+    const int j = lane + 64 * k;
+    bool kept;
+    if (m <= 0) kept = false;
+    else if (m >= nb) kept = true;
+    else kept = (s[k] > cut.s) || (s[k] == cut.s && j <= cut.j);
+    kept = kept && (j < nb);
+    if (j < nb) mrow[j] = kept ? 1 : 0;
+    const uint64_t bal = __ballot(kept);
+    if (kvrow && kept) kvrow[base + lanes_below(bal)] = j;
+    base += __popcll(bal);
+  }
+  if (lane == 0) *count_out = m;
+}
+
+template <int KPL>
+__global__ __launch_bounds__(1024) void select_kernel(const double* __restrict__ qbar,
+                                                     const double* __restrict__ kbar, int nb, double p, int k_min,
+                                                     uint8_t* __restrict__ mask, int32_t* __restrict__ counts,
+                                                     int32_t* __restrict__ kv_idx) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  double* sc = reinterpret_cast<double*>(smem);  // [kSelRows][nb]
+  WaveScratch* wsa = reinterpret_cast<WaveScratch*>(smem + sizeof(double) * kSelRows * nb);
+  const int bh = blockIdx.y;
+  const int i0 = blockIdx.x * kSelRows;
+  const int rows = min(kSelRows, nb - i0);
+  const double* qb = qbar + ((int64_t)bh * nb + i0) * kHeadDim;
+  const double* kb = kbar + (int64_t)bh * nb * kHeadDim;
+  const double inv_scale = 11.313708498984761;  // sqrt(128)
+
+  // Scores: one thread per key block, all rows of the workgroup at once.
+  for (int j = threadIdx.x; j < nb; j += blockDim.x) {
+    double acc[kSelRows];
+#pragma unroll
+    for (int r = 0; r < kSelRows; ++r) acc[r] = 0.0;
+    const double* kr = kb + (int64_t)j * kHeadDim;
+    for (int d = 0; d < kHeadDim; d += 2) {
+      const double2 kv = *reinterpret_cast<const double2*>(kr + d);
+#pragma unroll
+      for (int r = 0; r < kSelRows; ++r) {
+        const int rr = r < rows ? r : rows - 1;
+        acc[r] = fma(qb[rr * kHeadDim + d], kv.x, acc[r]);
+        acc[r] = fma(qb[rr * kHeadDim + d + 1], kv.y, acc[r]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kSelRows; ++r) sc[r * nb + j] = __ddiv_rn(acc[r], inv_scale);
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  for (int r = wave; r < rows; r += nwaves) {
+    const int64_t row = (int64_t)bh * nb + i0 + r;
+    select_row<KPL>(sc + r * nb, nb, p, k_min, mask + row * nb, counts + row, kv_idx ? kv_idx + row * nb : nullptr,
+                    wsa[wave], lane);
+  }
+}
+
+template <int KPL>
+hipError_t launch_select(const RouteArgs& a, int nb, double* qbar, double* kbar) {
+  const int bhs = a.batch * a.heads;
+  int threads = ((nb + 63) / 64) * 64;
+  if (threads > 1024) threads = 1024;
+  const size_t lds = sizeof(double) * kSelRows * nb + sizeof(WaveScratch) * (threads / 64);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<KPL>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  dim3 grid((nb + kSelRows - 1) / kSelRows, bhs);
+  hipLaunchKernelGGL(select_kernel<KPL>, grid, dim3(threads), lds, a.stream, qbar, kbar, nb, a.p, a.k_min, a.mask,
+                     a.counts, a.kv_idx);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t route_workspace_bytes(int batch, int heads, int nb) {
+  const size_t one = (size_t)batch * heads * nb * kHeadDim * sizeof(double);
+  const size_t aligned = (one + 255) & ~(size_t)255;
+  return 2 * aligned;
+}
+
+hipError_t launch_route(const RouteArgs& a) {
+  const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
+  const int bhs = a.batch * a.heads;
+  if (bhs == 0) return hipSuccess;
+  const size_t one = ((size_t)bhs * g.nb * kHeadDim * sizeof(double) + 255) & ~(size_t)255;
+  double* qbar = reinterpret_cast<double*>(a.workspace);
+  double* kbar = reinterpret_cast<double*>(reinterpret_cast<char*>(a.workspace) + one);
+  hipLaunchKernelGGL(pool_kernel, dim3(g.nb, bhs), dim3(kPoolThreads), 0, a.stream,
+                     reinterpret_cast<const uint16_t*>(a.Q), reinterpret_cast<const uint16_t*>(a.K), a.heads,
+                     a.stride_b, a.stride_h, a.stride_n, g, qbar, kbar);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int kpl = (g.nb + 63) / 64;
+  if (kpl <= 2) return launch_select<2>(a, g.nb, qbar, kbar);
+  if (kpl <= 4) return launch_select<4>(a, g.nb, qbar, kbar);
+  if (kpl <= 8) return launch_select<8>(a, g.nb, qbar, kbar);
+  return launch_select<16>(a, g.nb, qbar, kbar);
+}
+
+}  // namespace fva

@@ -1,0 +1,123 @@
+"""Host-side checks of the C ABI (no GPU needed, nothing is launched).
+
+* libfva.so loads and exports every function include/fva.h declares;
+* the host-only queries (block count, workspace sizes, trace size, status
+  strings) return the documented values;
+* every argument error is reported before any launch, with the documented
+  status: the calls below never reach a kernel, so fake device addresses
+  are safe.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_16190_amd as fva
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "fva.h")
+FAKE = ctypes.c_void_p(0x7F0000001000)  # 4 KiB aligned, never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fva_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert "fva_route" in names and "fva_attn" in names
+    lib = ctypes.CDLL(fva.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(fva.EXPORTED)
+
+
+def test_num_blocks():
+    assert fva.fva_num_blocks(fva.Tiling(3, 16, 16, 1, 8, 8)) == 12
+    assert fva.fva_num_blocks(fva.Tiling(21, 30, 52, 2, 8, 8)) == 308
+    assert fva.fva_num_blocks(fva.Tiling(21, 45, 80, 2, 8, 8)) == 660
+    assert fva.fva_num_blocks(fva.Tiling(31, 45, 80, 2, 8, 8)) == 960
+    assert fva.fva_num_blocks(fva.Tiling(0, 45, 80, 2, 8, 8)) == -1
+
+
+def desc(B=1, H=40, N=75600, D=128):
+    return fva._Desc(B, H, N, D, H * N * D, N * D, D)
+
+
+T720 = fva.Tiling(21, 45, 80, 2, 8, 8)
+
+
+def test_workspace_sizes():
+    nb = 660
+    rows = 40 * nb
+    assert fva.fva_route_workspace_size(desc(), T720) == 2 * rows * 128 * 8
+    al = lambda x: (x + 255) // 256 * 256
+    assert fva.fva_attn_workspace_size(desc(), T720) == al(rows * 4) + al(rows * nb * 4) + al(rows * 4) + al(4)
+    assert fva.fva_trace_words(desc(), T720) == rows * 4
+
+
+@pytest.mark.parametrize(
+    "d,t,status",
+    [
+        (desc(N=75601), T720, fva.FVA_ERR_SHAPE),
+        (desc(D=64), T720, fva.FVA_ERR_UNSUPPORTED),
+        (desc(N=21 * 45 * 80), fva.Tiling(21, 45, 80, 1, 4, 4), fva.FVA_ERR_UNSUPPORTED),  # tile volume 16
+        (desc(N=64 * 64 * 64), fva.Tiling(64, 64, 64, 2, 8, 8), fva.FVA_ERR_UNSUPPORTED),  # nb > 1024
+        (desc(), fva.Tiling(21, 45, 80, 0, 8, 8), fva.FVA_ERR_SHAPE),
+    ],
+)
+def test_shape_errors(d, t, status):
+    with pytest.raises(fva.FvaError) as e:
+        fva.fva_route_workspace_size(d, t)
+    assert e.value.status == status
+
+
+def _route(p=0.9, k_min=4, d=None, t=T720, q=FAKE, ws=FAKE, wsb=1 << 40, mask=FAKE, counts=FAKE):
+    d = d or desc()
+    return fva.lib.fva_route(q, FAKE, ctypes.byref(d), p, k_min, ctypes.byref(t.c()), mask, counts, None, ws,
+                             ctypes.c_size_t(wsb), None)
+
+
+def test_route_argument_errors():
+    assert _route(p=float("nan")) == fva.FVA_ERR_INVALID_ARG
+    assert _route(p=-0.01) == fva.FVA_ERR_INVALID_ARG
+    assert _route(p=1.5) == fva.FVA_ERR_INVALID_ARG
+    assert _route(k_min=-1) == fva.FVA_ERR_INVALID_ARG
+    assert _route(q=None) == fva.FVA_ERR_INVALID_ARG
+    assert _route(mask=None) == fva.FVA_ERR_INVALID_ARG
+    assert _route(counts=None) == fva.FVA_ERR_INVALID_ARG
+    assert _route(q=ctypes.c_void_p(0x7F0000001002)) == fva.FVA_ERR_INVALID_ARG  # misaligned rows
+    assert _route(ws=None) == fva.FVA_ERR_WORKSPACE
+    assert _route(wsb=100) == fva.FVA_ERR_WORKSPACE
+    assert _route(ws=ctypes.c_void_p(0x7F0000001080)) == fva.FVA_ERR_WORKSPACE  # not 256-aligned
+    assert _route(d=desc(N=10)) == fva.FVA_ERR_SHAPE
+    bad = desc()
+    bad.stride_n = 100  # rows overlap and are not 16-byte aligned
+    assert _route(d=bad) == fva.FVA_ERR_SHAPE
+
+
+def _attn(flags=0, counts=None, kv=None, mask=FAKE, trace=None, scale=0.0, ws=FAKE, wsb=1 << 40, o=FAKE):
+    d = desc()
+    return fva.lib.fva_attn(FAKE, FAKE, FAKE, ctypes.byref(d), ctypes.byref(T720.c()), mask, counts, kv,
+                            ctypes.c_float(scale), flags, o, ws, ctypes.c_size_t(wsb), trace, None)
+
+
+def test_attn_argument_errors():
+    assert _attn(flags=8) == fva.FVA_ERR_INVALID_ARG
+    assert _attn(counts=FAKE, kv=None) == fva.FVA_ERR_INVALID_ARG
+    assert _attn(counts=None, kv=FAKE) == fva.FVA_ERR_INVALID_ARG
+    assert _attn(mask=None) == fva.FVA_ERR_INVALID_ARG
+    assert _attn(flags=fva.FVA_TRACE, trace=None) == fva.FVA_ERR_INVALID_ARG
+    assert _attn(scale=float("nan")) == fva.FVA_ERR_INVALID_ARG
+    assert _attn(o=None) == fva.FVA_ERR_INVALID_ARG
+    assert _attn(wsb=10) == fva.FVA_ERR_WORKSPACE
+
+
+def test_status_strings():
+    assert fva.fva_status_string(0) == "ok"
+    for s in (-1, -2, -3, -4, -5):
+        assert fva.fva_status_string(s) != "unknown status"
+    assert fva.fva_status_string(7) == "unknown status"

@@ -1,0 +1,190 @@
+"""GPU parity of fva_attn against the fp64 oracle, on the same mask.
+
+Bar: max |O_gpu - O_ref| <= 2e-2 and mean <= 1e-3 over compared real-token
+elements. Small workloads compare every element; the full-size workloads
+compare sampled query blocks (the lowest- and highest-density heads, two
+more heads, plus random rows) in the launch configuration the benchmark
+times (persistent scheduler, kept-block lists from fva_route).
+"""
+
+import zlib
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import attn_ref_head, attn_ref_rows
+from oracle.compare import ATTN_MAX_ABS, ATTN_MEAN_ABS, attn_errors
+
+from _gpu_util import custom_config, f64, geometry_of, lib, log, tiling_of, to_dev, torch_mod, workload
+
+pytestmark = pytest.mark.gpu
+
+
+def upload(Qb, Kb, Vb):
+    return to_dev(Qb), to_dev(Kb), to_dev(Vb)
+
+
+def run_attn(q, k, v, cfg, mask_t, counts_t=None, kv_t=None, flags=0, scale=0.0):
+    fva = lib()
+    out = fva.fva_attn(q, k, v, tiling_of(cfg), mask_t, counts_t, kv_t, flags=flags, scale=scale)
+    torch_mod().cuda.synchronize()
+    return out
+
+
+def o64(out):
+    return out.float().cpu().numpy().astype(np.float64)
+
+
+def compare_full(name, Qb, Kb, Vb, cfg, mask, O, scale=None):
+    geo = geometry_of(cfg)
+    errs = []
+    for b in range(Qb.shape[0]):
+        for h in range(Qb.shape[1]):
+            ref = attn_ref_head(f64(Qb[b, h]), f64(Kb[b, h]), f64(Vb[b, h]), mask[b, h], geo, scale)
+            errs.append(np.abs(O[b, h] - ref))
+    e = np.concatenate([x.ravel() for x in errs])
+    log(f"[attn] {name}: max abs {e.max():.3e} mean abs {e.mean():.3e} over {e.size} elements")
+    assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
+    return e.max(), e.mean()
+
+
+def test_attn_tiny_routed_mask_both_schedulers():
+    fva = lib()
+    cfg = synth.get_config("tiny")
+    Qb, Kb, Vb = workload("tiny")
+    q, k, v = upload(Qb, Kb, Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    O_p = run_attn(q, k, v, cfg, mask, counts, kv, flags=fva.FVA_SCHED_PERSISTENT)
+    O_n = run_attn(q, k, v, cfg, mask, counts, kv, flags=fva.FVA_SCHED_NAIVE)
+    O_m = run_attn(q, k, v, cfg, mask)  # counts / kv_idx rebuilt from the mask
+    assert torch_mod().equal(O_p, O_n) and torch_mod().equal(O_p, O_m)
+    compare_full("tiny", Qb, Kb, Vb, cfg, mask.cpu().numpy(), o64(O_p))
+
+
+MASK_KINDS = ["ones", "diagonal", "random30", "random70", "edge_only", "empty_rows"]
+
+
+def make_mask(kind, B, H, nb, geo, rng):
+    if kind == "ones":
+        return np.ones((B, H, nb, nb), np.uint8)
+    if kind == "diagonal":
+        m = np.zeros((B, H, nb, nb), np.uint8)
+        m[..., np.arange(nb), np.arange(nb)] = 1
+        return m
+    if kind.startswith("random"):
+        dens = int(kind[6:]) / 100
+        m = (rng.uniform(size=(B, H, nb, nb)) < dens).astype(np.uint8)
+        m[..., np.arange(nb), rng.integers(0, nb, nb)] = 1
+        return m
+    if kind == "edge_only":
+        small = geo.block_sizes < geo.block_sizes.max()
+        m = np.zeros((B, H, nb, nb), np.uint8)
+        m[..., :, small] = 1
+        m[..., :, 0] = 1
+        return m
+    if kind == "empty_rows":
+        m = (rng.uniform(size=(B, H, nb, nb)) < 0.5).astype(np.uint8)
+        m[..., ::3, :] = 0
+        return m
+    raise ValueError(kind)
+
+
+@pytest.mark.parametrize("kind", MASK_KINDS)
+@pytest.mark.parametrize("grid,tile", [((5, 13, 21), (2, 8, 8)), ((3, 9, 10), (1, 8, 8)), ((3, 16, 16), (1, 8, 8))])
+def test_attn_host_masks(kind, grid, tile):
+    torch = torch_mod()
+    fva = lib()
+    cfg = custom_config("masks", 2, grid, tile, (0.5, 3.0), seed=21)
+    geo = geometry_of(cfg)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    mask = make_mask(kind, 1, 2, geo.nb, geo, np.random.default_rng(zlib.crc32(repr((kind, grid)).encode())))
+    q, k, v = upload(Qb, Kb, Vb)
+    mt = torch.from_numpy(mask).to("cuda:0")
+    O = run_attn(q, k, v, cfg, mt)
+    O_n = run_attn(q, k, v, cfg, mt, flags=fva.FVA_SCHED_NAIVE)
+    assert torch.equal(O, O_n)
+    Of = o64(O)
+    compare_full(f"{kind} grid{grid}", Qb, Kb, Vb, cfg, mask, Of)
+    if kind == "empty_rows":
+        for i in range(0, geo.nb, 3):
+            assert np.all(Of[:, :, geo.block_tokens[i]] == 0)
+
+
+def test_attn_custom_scale_and_strided_layout():
+    torch = torch_mod()
+    cfg = custom_config("strided", 3, (3, 9, 10), (1, 8, 8), (0.5, 1.0, 3.0), seed=22)
+    geo = geometry_of(cfg)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    # [B, N, H, d] storage viewed as [B, H, N, d]
+    def bnhd(bits):
+        t = to_dev(np.ascontiguousarray(bits.transpose(0, 2, 1, 3)))
+        return t.permute(0, 2, 1, 3)
+    q, k, v = bnhd(Qb), bnhd(Kb), bnhd(Vb)
+    assert q.stride(1) == 128 and q.stride(2) == 3 * 128
+    mask = make_mask("random30", 1, 3, geo.nb, geo, np.random.default_rng(5))
+    O = run_attn(q, k, v, cfg, torch.from_numpy(mask).to("cuda:0"), scale=0.05)
+    compare_full("strided scale=0.05", Qb, Kb, Vb, cfg, mask, o64(O), scale=0.05)
+
+
+def sampled_rows(counts, nb, rng, n_random=32, per_head=8):
+    """(h, i) pairs: 4 heads (min, max density, two random) x per_head rows, plus random rows."""
+    dens = counts.mean(axis=-1)
+    H = counts.shape[0]
+    heads = [int(np.argmin(dens)), int(np.argmax(dens))]
+    heads += [int(h) for h in rng.choice([h for h in range(H) if h not in heads], 2, replace=False)]
+    pairs = set()
+    for h in heads:
+        for i in rng.choice(nb, per_head, replace=False):
+            pairs.add((h, int(i)))
+    while len(pairs) < len(heads) * per_head + n_random:
+        pairs.add((int(rng.integers(H)), int(rng.integers(nb))))
+    return sorted(pairs)
+
+
+@pytest.mark.parametrize("name", ["480p", "720p", "720p_stress", "long"])
+def test_attn_full_workloads_sampled(name):
+    fva = lib()
+    cfg = synth.get_config(name)
+    geo = geometry_of(cfg)
+    Qb, Kb, Vb = workload(name)
+    q, k, v = upload(Qb, Kb, Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    O = run_attn(q, k, v, cfg, mask, counts, kv)
+    m = mask.cpu().numpy()[0]
+    c = counts.cpu().numpy()[0]
+    rng = np.random.default_rng(31)
+    pairs = sampled_rows(c, geo.nb, rng)
+    Of = O[0].float().cpu().numpy()
+    errs = []
+    by_head = {}
+    for h, i in pairs:
+        by_head.setdefault(h, []).append(i)
+    for h, rows in by_head.items():
+        ref = attn_ref_rows(f64(Qb[0, h]), f64(Kb[0, h]), f64(Vb[0, h]), m[h], geo, rows)
+        for i, o in ref.items():
+            errs.append(np.abs(Of[h][geo.block_tokens[i]] - o).ravel())
+    e = np.concatenate(errs)
+    log(f"[attn] {name}: {len(pairs)} sampled rows, max abs {e.max():.3e} mean abs {e.mean():.3e}, "
+        f"density {c.mean() / geo.nb:.3f}")
+    assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
+
+
+def test_attn_deterministic_and_trace():
+    torch = torch_mod()
+    fva = lib()
+    cfg = synth.get_config("720p")
+    geo = geometry_of(cfg)
+    Qb, Kb, Vb = workload("720p")
+    q, k, v = upload(Qb, Kb, Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    O1 = run_attn(q, k, v, cfg, mask, counts, kv)
+    desc = fva._desc_of(q)
+    trace = torch.zeros(fva.fva_trace_words(desc, tiling_of(cfg)), dtype=torch.int64, device="cuda:0")
+    O2 = fva.fva_attn(q, k, v, tiling_of(cfg), mask, counts, kv, flags=fva.FVA_TRACE, trace=trace)
+    O3 = run_attn(q, k, v, cfg, mask, counts, kv, flags=fva.FVA_SCHED_NAIVE)
+    torch.cuda.synchronize()
+    assert torch.equal(O1, O2) and torch.equal(O1, O3)
+    tr = trace.view(-1, 4).cpu().numpy()
+    assert tr.shape[0] == cfg.heads * geo.nb
+    assert np.all(tr[:, 1] >= tr[:, 0]) and np.all(tr[:, 0] > 0)
