@@ -82,6 +82,11 @@ class FvaError(RuntimeError):
 
 
 def _load():
+    # torch ships its own HIP runtime under the same soname; loading torch
+    # first makes libfva.so bind to that runtime, so device pointers and
+    # streams from torch are valid in the library's launches.
+    import torch  # noqa: F401
+
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"{LIB_PATH} is missing: build the HIP library first "

@@ -406,6 +406,7 @@ size_t attn_workspace_bytes(int batch, int heads, int nb) {
 }
 
 hipError_t launch_attn(const AttnArgs& a) {
+  (void)hipGetLastError();  // drop an error left by an unrelated earlier HIP call
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
   const int n_items = a.batch * a.heads * g.nb;
   if (n_items == 0) return hipSuccess;

@@ -394,6 +394,7 @@ size_t route_workspace_bytes(int batch, int heads, int nb) {
 }
 
 hipError_t launch_route(const RouteArgs& a) {
+  (void)hipGetLastError();  // drop an error left by an unrelated earlier HIP call
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
   const int bhs = a.batch * a.heads;
   if (bhs == 0) return hipSuccess;

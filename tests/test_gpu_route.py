@@ -87,7 +87,7 @@ def test_route_partial_tiles(grid, tile, p, k_min):
 
 
 @pytest.mark.parametrize("grid", [(3, 16, 16), (4, 32, 40), (10, 40, 48)])
-@pytest.mark.parametrize("p,k_min", [(0.9, 2), (0.55, 0), (0.3, 7)])
+@pytest.mark.parametrize("p,k_min", [(0.9037, 2), (0.5513, 0), (0.3071, 7)])  # p*nb never integral
 def test_route_exact_ties(grid, p, k_min):
     # Q = 0: every score is exactly 0, P = 1/nb, the kept set is the lowest
     # m = max(ceil(p*nb), k_min) block ids (ties go to the lower id).
