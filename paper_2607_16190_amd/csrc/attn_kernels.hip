@@ -32,11 +32,12 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kAttnThreads = 256;
-constexpr int kLdsStride = 136;  // bf16 per LDS row: 128 + 8 padding (272 B) keeps MFMA reads conflict-free
-constexpr int kTileElems = 128 * kLdsStride;
-constexpr size_t kAttnLds = 2 * kTileElems * sizeof(uint16_t);
+constexpr int kRowBytes = 256;                 // one 128-dim bf16 row
+constexpr int kTileBytes = 128 * kRowBytes;    // 32 KB per K or V tile
 
 struct AttnParams {
   const uint16_t* Q;
@@ -52,14 +53,42 @@ struct AttnParams {
   int64_t* trace;
 };
 
-// LDS row of key kap: keys 32kg + 8g + e (e < 8) land on rows
-// 32kg + 16*(e/4) + 4g + e%4, i.e. the S^T accumulator of lane group g in
-// tiles 2kg and 2kg+1 holds keys 32kg + 8g .. 32kg + 8g + 7 in order.
-__device__ __forceinline__ int k_lds_row(int kap) {
-  const int kg = kap >> 5;
-  const int g = (kap >> 3) & 3;
-  const int e = kap & 7;
-  return (kg << 5) | ((e >> 2) << 4) | (g << 2) | (e & 3);
+// LDS row order of a K / V tile. Key kap = 32kg + 8g + 4hh + r is stored in
+// row 32kg + 16hh + 4g + r, so that the S^T accumulator rows held by lane
+// group g in tiles 2kg and 2kg+1 are the 8 consecutive keys 32kg + 8g + 0..7
+// (the B operand of the PV product), and the 16 rows read by one transposing
+// V load are consecutive.
+__device__ __forceinline__ int key_of_row(int rho) {
+  return ((rho >> 5) << 5) | (((rho >> 2) & 3) << 3) | (((rho >> 4) & 1) << 2) | (rho & 3);
+}
+
+// Uniform per-block constants for mapping a packed row index to its token.
+struct BlockMap {
+  int tbase;      // token of the box origin
+  int plane, ex;  // ey*ex and ex
+  int mp, mx;     // ceil(2^16 / plane), ceil(2^16 / ex): exact quotients for rows < 128
+  int n;          // real tokens
+};
+
+__device__ __forceinline__ BlockMap block_map(const Geometry& g, int j) {
+  const BlockBox b = block_box(g, j);
+  BlockMap m;
+  m.tbase = (b.t0 * g.H + b.y0) * g.W + b.x0;
+  m.plane = b.ey * b.ex;
+  m.ex = b.ex;
+  m.mp = (65536 + m.plane - 1) / m.plane;
+  m.mx = (65536 + m.ex - 1) / m.ex;
+  m.n = b.n;
+  return m;
+}
+
+// Token of packed row r (< 128) of a block: 24-bit multiplies only.
+__device__ __forceinline__ int row_token(const BlockMap& m, int r, int HW, int W) {
+  const int lt = (int)(__umul24(r, m.mp) >> 16);
+  const int rem = r - (int)__umul24(lt, m.plane);
+  const int ly = (int)(__umul24(rem, m.mx) >> 16);
+  const int lx = rem - (int)__umul24(ly, m.ex);
+  return m.tbase + (int)__umul24(lt, HW) + (int)__umul24(ly, W) + lx;
 }
 
 __device__ __forceinline__ uint32_t hw_location() {
@@ -69,39 +98,59 @@ __device__ __forceinline__ uint32_t hw_location() {
   return ((xcc & 0xffu) << 16) | (hw & 0xffffu);
 }
 
-__device__ __forceinline__ void load_kv_regs(const AttnParams& P, int64_t base, int j, uint4 (&kr)[8],
-                                             uint4 (&vr)[8]) {
-  const BlockBox bj = block_box(P.g, j);
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Row element offsets (relative to the head base) of the 8 LDS rows this
+// lane fills: wave w fills rows 32w .. 32w+31 (key group w), four rows per
+// load instruction. Padding rows repeat the last real row (finite values;
+// their scores are masked).
+__device__ __forceinline__ void row_offsets(const AttnParams& P, const BlockMap& m, int (&roff)[8]) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int HW = P.g.H * P.g.W;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
-    const int it = threadIdx.x + kAttnThreads * u;
-    const int kap = it >> 4;
-    const int cc = it & 15;
-    if (kap < bj.n) {
-      const int64_t off = base + (int64_t)box_token(P.g, bj, kap) * P.sn + cc * 8;
-      kr[u] = *reinterpret_cast<const uint4*>(P.K + off);
-      vr[u] = *reinterpret_cast<const uint4*>(P.V + off);
-    } else {
-      kr[u] = make_uint4(0, 0, 0, 0);
-      vr[u] = make_uint4(0, 0, 0, 0);
-    }
+    const int rho = w * 32 + u * 4 + (lane >> 4);
+    const int kap = min(key_of_row(rho), m.n - 1);
+    roff[u] = row_token(m, kap, HW, P.g.W) * (int)P.sn;
   }
 }
 
-__device__ __forceinline__ void store_kv_lds(uint16_t* __restrict__ Ks, uint16_t* __restrict__ Vt,
-                                             const uint4 (&kr)[8], const uint4 (&vr)[8]) {
+// Asynchronous global -> LDS copy of this wave's 8 KB of a tile. K rows use a
+// 16-byte-chunk XOR swizzle (chunk ^ row%16), V rows an 8-byte-chunk swizzle
+// (chunk8 ^ 4*(row%8)); both make the MFMA-side reads bank-conflict free.
+// Asynchronous global -> LDS copy of this wave's 8 KB of a tile. K rows use a
+// 16-byte-chunk XOR swizzle (chunk ^ row%16), V rows an 8-byte-chunk swizzle
+// (chunk8 ^ 4*(row%8)); both make the MFMA-side reads bank-conflict free.
+// The copies are issued from inline assembly so that the compiler does not
+// drain them (vmcnt(0)) before unrelated LDS reads; the kernel waits for them
+// explicitly (wait_vmem) before the barrier that publishes a tile. M0 holds
+// the LDS destination; nothing else in these kernels uses M0.
+template <bool IS_V>
+__device__ __forceinline__ void issue_tile(const uint16_t* __restrict__ src, const int (&roff)[8],
+                                           unsigned char* tile) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int p = lane & 15;
+  const int lq = lane >> 4;
+  const unsigned char* gbase = reinterpret_cast<const unsigned char*>(src);  // wave-uniform
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)tile;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
-    const int it = threadIdx.x + kAttnThreads * u;
-    const int kap = it >> 4;
-    const int cc = it & 15;
-    *reinterpret_cast<uint4*>(Ks + k_lds_row(kap) * kLdsStride + cc * 8) = kr[u];
-    const uint32_t w[4] = {vr[u].x, vr[u].y, vr[u].z, vr[u].w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      Vt[(cc * 8 + 2 * e) * kLdsStride + kap] = (uint16_t)(w[e] & 0xffffu);
-      Vt[(cc * 8 + 2 * e + 1) * kLdsStride + kap] = (uint16_t)(w[e] >> 16);
-    }
+    // rho = 32w + 4u + lq, so rho % 16 = 4(u % 4) + lq and rho % 8 = 4(u % 2) + lq
+    const int chunk = IS_V ? (p ^ (2 * (4 * (u & 1) + lq))) : (p ^ (4 * (u & 3) + lq));
+    const uint32_t off = (uint32_t)roff[u] * 2u + 16u * (uint32_t)chunk;
+    const uint32_t dst = lds0 + (uint32_t)((w * 8 + u) * 1024);
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(dst), "v"(off), "s"(gbase)
+                 : "memory");
   }
 }
 
@@ -110,22 +159,39 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 a, f32x4 b) {
   return __builtin_convertvector(v, bf16x8);
 }
 
-__device__ void process_item(const AttnParams& P, int item, uint16_t* __restrict__ lds) {
-  uint16_t* Ks = lds;
-  uint16_t* Vt = lds + kTileElems;
+__device__ __forceinline__ int ngroups_of(int n) { return (n + 31) >> 5; }
+
+// Workgroup barrier without a memory fence: the only cross-wave traffic in
+// the block loop is the LDS tiles written by global->LDS copies, and every
+// wave waits for its own copies (vmcnt) before arriving here.
+__device__ __forceinline__ void tile_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+__device__ void process_item(const AttnParams& P, int item, unsigned char* __restrict__ Ks,
+                             unsigned char* __restrict__ Vs) {
   const int nb = P.g.nb;
   const int bh = item / nb;
   const int i = item - bh * nb;
   const int b = bh / P.heads;
   const int h = bh - b * P.heads;
   const int64_t base = (int64_t)b * P.sb + (int64_t)h * P.sh;
+  const uint16_t* Qh = P.Q + base;
+  const uint16_t* Kh = P.K + base;
+  const uint16_t* Vh = P.V + base;
+  uint16_t* Oh = P.O + base;
   const BlockBox bi = block_box(P.g, i);
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g4 = lane >> 4;
   const int l16 = lane & 15;
   const int row0 = wave * 32;
   const bool active = row0 < bi.n;
+
+  // counts and kv_idx are read through the scalar cache (constant address
+  // space: the kernel never writes them). They come from the caller: clamp
+  // so a bad list cannot address outside the tensors.
+  typedef __attribute__((address_space(4))) const int32_t const_i32;
+  const const_i32* kvl = (const const_i32*)(P.kv_idx + (int64_t)item * nb);
+  const int cnt = min(max(((const const_i32*)P.counts)[item], 0), nb);
 
   // Q_i^T as the B operand: lane holds query row l16 of each 16-row tile,
   // head dims 32ks + 8g4 .. +7.
@@ -138,12 +204,16 @@ __device__ void process_item(const AttnParams& P, int item, uint16_t* __restrict
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       if (qtok[nt] >= 0) {
-        qf[nt][ks] = *reinterpret_cast<const bf16x8*>(P.Q + base + (int64_t)qtok[nt] * P.sn + 32 * ks + 8 * g4);
+        qf[nt][ks] = *reinterpret_cast<const bf16x8*>(Qh + (uint32_t)(qtok[nt] * (int)P.sn + 32 * ks + 8 * g4));
       } else {
         qf[nt][ks] = bf16x8{};
       }
     }
   }
+
+  // Q is in registers before any tile copy is issued (a wait the compiler
+  // sees, so it never re-waits for Q behind the copies).
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt/lgkmcnt unconstrained
 
   f32x4 o[8][2];
 #pragma unroll
@@ -153,110 +223,194 @@ __device__ void process_item(const AttnParams& P, int item, uint16_t* __restrict
   float mrow[2] = {-1.0e30f, -1.0e30f};
   float lrow[2] = {0.f, 0.f};
 
-  // counts and kv_idx come from the caller: clamp so a bad list cannot
-  // address outside the tensors.
-  const int cnt = min(max(P.counts[item], 0), nb);
-  const int32_t* kvl = P.kv_idx + (int64_t)item * nb;
-  uint4 kr[8], vr[8];
-  int jn = cnt > 0 ? min(max(kvl[0], 0), nb - 1) : 0;
-  if (cnt > 0) load_kv_regs(P, base, jn, kr, vr);
+  // Lane constants of the transposing V reads: source lane 4e + q of group g4
+  // points at row 32kg + 16hf + 4g4 + e, 8-byte chunk 4mt + q (swizzled).
+  const int te = l16 >> 2;
+  const int tq = l16 & 3;
+  const int vrow = (4 * g4 + te) * kRowBytes;
+  const int vsw = (4 * g4 + te) & 7;
+
+  int roff[8];
+  int jc = cnt > 0 ? min(max(kvl[0], 0), nb - 1) : 0;
+  BlockMap mc = block_map(P.g, jc);
+  if (cnt > 0) {
+    row_offsets(P, mc, roff);
+    if (wave < ngroups_of(mc.n)) {
+      issue_tile<false>(Kh, roff, Ks);
+      issue_tile<true>(Vh, roff, Vs);
+    }
+  }
+
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  auto vfrag = [&](int kg, int mt) {
+    const unsigned char* vb = Vs + kg * 32 * kRowBytes + vrow + 8 * (4 * (mt ^ vsw) + tq);
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds_void*)vb);
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds_void*)(vb + 16 * kRowBytes));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  auto kfrag = [&](int mt, int ks) {
+    return *reinterpret_cast<const bf16x8*>(Ks + (mt * 16 + l16) * kRowBytes + 16 * ((4 * ks + g4) ^ l16));
+  };
 
   for (int c = 0; c < cnt; ++c) {
-    const int nj = block_box(P.g, jn).n;
-    __syncthreads();
-    store_kv_lds(Ks, Vt, kr, vr);
-    __syncthreads();
-    if (c + 1 < cnt) {
-      jn = min(max(kvl[c + 1], 0), nb - 1);
-      load_kv_regs(P, base, jn, kr, vr);
-    }
-    if (!active) continue;
-    const int ngroups = (nj + 31) >> 5;
+    const int nj = mc.n;
+    const int ng = ngroups_of(nj);
+    // K_c landed (V_c, issued after it, may still be in flight).
+    if (wave < ng) wait_vmem<8>(); else wait_vmem<0>();
+    tile_barrier();
 
-    // S^T = K Q^T over the key tiles that hold real keys.
-    f32x4 s[8][2];
+    int ng_next = 0;
+    // Each 128-key block is taken as two halves of 64 keys (key groups 2hb,
+    // 2hb+1): S half -> online softmax -> PV half. Half 1 of a block with at
+    // most 64 real keys is empty.
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt) {
-      if (mt < 2 * ngroups) {
-        s[mt][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-        s[mt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int hb = 0; hb < 2; ++hb) {
+      const int ngh = min(max(ng - 2 * hb, 0), 2);  // key groups in this half
+      f32x4 s[4][2];
+      if (active && ngh > 0) {
+        // S^T = K Q^T for LDS tiles 4hb .. 4hb + 2ngh - 1; the fragments of
+        // tile t+1 load while tile t multiplies.
+        bf16x8 ka[4], kn[4];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(Ks + (mt * 16 + l16) * kLdsStride + 32 * ks + 8 * g4);
-          s[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], s[mt][0], 0, 0, 0);
-          s[mt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], s[mt][1], 0, 0, 0);
+        for (int ks = 0; ks < 4; ++ks) ka[ks] = kfrag(4 * hb, ks);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          if (t < 2 * ngh) {
+            if (t + 1 < 2 * ngh) {
+#pragma unroll
+              for (int ks = 0; ks < 4; ++ks) kn[ks] = kfrag(4 * hb + t + 1, ks);
+            }
+            s[t][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+            s[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+              s[t][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qf[0][ks], s[t][0], 0, 0, 0);
+              s[t][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qf[1][ks], s[t][1], 0, 0, 0);
+            }
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) ka[ks] = kn[ks];
+            __builtin_amdgcn_sched_barrier(0);
+          }
         }
       }
-    }
+      if (hb == 1) {
+        tile_barrier();  // every wave is done with K_c
+        // Next block's K streams in while this block finishes.
+        if (c + 1 < cnt) {
+          const int jn = min(max(kvl[c + 1], 0), nb - 1);
+          mc = block_map(P.g, jn);
+          ng_next = ngroups_of(mc.n);
+          if (wave < ng_next) {
+            row_offsets(P, mc, roff);
+            issue_tile<false>(Kh, roff, Ks);
+          }
+        }
+      }
 
-    // Online softmax; key of accumulator (mt, r) in lane group g4 is
-    // 32*(mt/2) + 8*g4 + 4*(mt%2) + r.
-    float mx[2] = {-INFINITY, -INFINITY};
+      bf16x8 pb[2][2];
+      if (active && ngh > 0) {
+        // Online softmax over this half. Accumulator (t, r) of lane group g4
+        // holds key 64hb + 32*(t/2) + 8*g4 + 4*(t%2) + r.
+        if (nj < 64 * hb + 32 * ngh) {
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt) {
-      if (mt < 2 * ngroups) {
+          for (int t = 0; t < 4; ++t) {
+            if (t < 2 * ngh) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int kap = 32 * (mt >> 1) + 8 * g4 + 4 * (mt & 1) + r;
+              for (int r = 0; r < 4; ++r) {
+                const int kap = 64 * hb + 32 * (t >> 1) + 8 * g4 + 4 * (t & 1) + r;
+                if (kap >= nj) {
+                  s[t][0][r] = -INFINITY;
+                  s[t][1][r] = -INFINITY;
+                }
+              }
+            }
+          }
+        }
+        float mx[2] = {-INFINITY, -INFINITY};
 #pragma unroll
-          for (int nt = 0; nt < 2; ++nt) {
-            const float v = kap < nj ? s[mt][nt][r] : -INFINITY;
-            s[mt][nt][r] = v;
-            mx[nt] = fmaxf(mx[nt], v);
+        for (int t = 0; t < 4; ++t) {
+          if (t < 2 * ngh) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              mx[0] = fmaxf(mx[0], s[t][0][r]);
+              mx[1] = fmaxf(mx[1], s[t][1][r]);
+            }
+          }
+        }
+        float alpha[2], negm[2];
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          mx[nt] = fmaxf(mx[nt], __shfl_xor(mx[nt], 16));
+          mx[nt] = fmaxf(mx[nt], __shfl_xor(mx[nt], 32));
+          const float mnew = fmaxf(mrow[nt], mx[nt]);
+          negm[nt] = -mnew * P.c2;
+          alpha[nt] = __builtin_amdgcn_exp2f(fmaf(mrow[nt], P.c2, negm[nt]));
+          mrow[nt] = mnew;
+        }
+        float rs[2] = {0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          if (kk < ngh) {
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              const int t = 2 * kk + hh;
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt) {
+                  const float pv = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
+                  s[t][nt][r] = pv;
+                  rs[nt] += pv;
+                }
+              }
+            }
+            pb[kk][0] = to_bf16x8(s[2 * kk][0], s[2 * kk + 1][0]);
+            pb[kk][1] = to_bf16x8(s[2 * kk][1], s[2 * kk + 1][1]);
+          }
+        }
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          rs[nt] += __shfl_xor(rs[nt], 16);
+          rs[nt] += __shfl_xor(rs[nt], 32);
+          lrow[nt] = lrow[nt] * alpha[nt] + rs[nt];
+          // Once the running max stops moving, alpha == 1 exactly and the
+          // rescale is skipped.
+          if (__ballot(alpha[nt] != 1.0f)) {
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha[nt];
+          }
+        }
+      }
+
+      if (hb == 0) {
+        // V_c landed: nothing was issued after it yet.
+        wait_vmem<0>();
+        tile_barrier();
+      }
+
+      if (active && ngh > 0) {
+        // O^T += V^T P^T, 32 keys per MFMA; V^T comes from row-major V through
+        // transposing LDS reads; step t+1's fragment loads while step t runs.
+        bf16x8 va = vfrag(2 * hb, 0);
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          if (kk < ngh) {
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) {
+              bf16x8 vn = va;
+              if (mt + 1 < 8) vn = vfrag(2 * hb + kk, mt + 1);
+              else if (kk + 1 < ngh) vn = vfrag(2 * hb + kk + 1, 0);
+              o[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][0], o[mt][0], 0, 0, 0);
+              o[mt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][1], o[mt][1], 0, 0, 0);
+              va = vn;
+              __builtin_amdgcn_sched_barrier(0);
+            }
           }
         }
       }
     }
-    float alpha[2], negmc[2];
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      mx[nt] = fmaxf(mx[nt], __shfl_xor(mx[nt], 16));
-      mx[nt] = fmaxf(mx[nt], __shfl_xor(mx[nt], 32));
-      const float mnew = fmaxf(mrow[nt], mx[nt]);
-      alpha[nt] = exp2f((mrow[nt] - mnew) * P.c2);
-      mrow[nt] = mnew;
-      negmc[nt] = -mnew * P.c2;
-    }
-    float rs[2] = {0.f, 0.f};
-#pragma unroll
-    for (int mt = 0; mt < 8; ++mt) {
-      if (mt < 2 * ngroups) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-#pragma unroll
-          for (int nt = 0; nt < 2; ++nt) {
-            const float pv = exp2f(fmaf(s[mt][nt][r], P.c2, negmc[nt]));
-            s[mt][nt][r] = pv;
-            rs[nt] += pv;
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      rs[nt] += __shfl_xor(rs[nt], 16);
-      rs[nt] += __shfl_xor(rs[nt], 32);
-      lrow[nt] = lrow[nt] * alpha[nt] + rs[nt];
-    }
-#pragma unroll
-    for (int mt = 0; mt < 8; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) o[mt][nt] *= alpha[nt];
-
-    // O^T += V^T P^T, 32 keys per MFMA.
-#pragma unroll
-    for (int kg = 0; kg < 4; ++kg) {
-      if (kg < ngroups) {
-        const bf16x8 p0 = to_bf16x8(s[2 * kg][0], s[2 * kg + 1][0]);
-        const bf16x8 p1 = to_bf16x8(s[2 * kg][1], s[2 * kg + 1][1]);
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(Vt + (mt * 16 + l16) * kLdsStride + 32 * kg + 8 * g4);
-          o[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p0, o[mt][0], 0, 0, 0);
-          o[mt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p1, o[mt][1], 0, 0, 0);
-        }
-      }
-    }
+    tile_barrier();  // every wave is done with V_c
+    if (c + 1 < cnt && wave < ng_next) issue_tile<true>(Vh, roff, Vs);
   }
 
   // Epilogue: O^T accumulator (mt, r) of lane (g4, l16) is head dim
@@ -266,7 +420,7 @@ __device__ void process_item(const AttnParams& P, int item, uint16_t* __restrict
     for (int nt = 0; nt < 2; ++nt) {
       if (qtok[nt] >= 0) {
         const float inv = lrow[nt] > 0.f ? 1.0f / lrow[nt] : 0.f;
-        uint16_t* orow = P.O + base + (int64_t)qtok[nt] * P.sn + 4 * g4;
+        uint16_t* orow = Oh + (uint32_t)(qtok[nt] * (int)P.sn + 4 * g4);
 #pragma unroll
         for (int mt = 0; mt < 8; ++mt) {
           const f32x4 v = o[mt][nt] * inv;
@@ -288,29 +442,32 @@ __device__ __forceinline__ void trace_item(const AttnParams& P, int item, int64_
   }
 }
 
-__global__ __launch_bounds__(kAttnThreads, 1) void attn_naive_kernel(AttnParams P) {
-  extern __shared__ __align__(16) uint16_t lds[];
+__global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams P) {
+  __shared__ __align__(16) unsigned char ks_tile[kTileBytes];
+  __shared__ __align__(16) unsigned char vs_tile[kTileBytes];
   const int64_t t0 = (int64_t)wall_clock64();
-  process_item(P, blockIdx.x, lds);
+  process_item(P, blockIdx.x, ks_tile, vs_tile);
   if (P.trace) {
     __syncthreads();
     trace_item(P, blockIdx.x, t0);
   }
 }
 
-__global__ __launch_bounds__(kAttnThreads, 1) void attn_persistent_kernel(AttnParams P, const int32_t* __restrict__ items,
+__global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnParams P, const int32_t* __restrict__ items,
                                                                           int n_items, int32_t* __restrict__ counter) {
-  extern __shared__ __align__(16) uint16_t lds[];
+  __shared__ __align__(16) unsigned char ks_tile[kTileBytes];
+  __shared__ __align__(16) unsigned char vs_tile[kTileBytes];
   __shared__ int next;
   for (;;) {
     __syncthreads();
     if (threadIdx.x == 0) next = atomicAdd(counter, 1);
     __syncthreads();
-    const int slot = next;
+    const int slot = __builtin_amdgcn_readfirstlane(next);
     if (slot >= n_items) break;
-    const int item = items[slot];
+    const int item = __builtin_amdgcn_readfirstlane(items[slot]);
     const int64_t t0 = (int64_t)wall_clock64();
-    process_item(P, item, lds);
+    process_item(P, item, ks_tile, vs_tile);
+    __syncthreads();  // the next item's copies overwrite the tiles
     if (P.trace) {
       __syncthreads();
       trace_item(P, item, t0);
@@ -382,13 +539,8 @@ hipError_t device_info(DeviceInfo& info) {
     DeviceInfo d;
     e = hipDeviceGetAttribute(&d.cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    for (const void* fn : {reinterpret_cast<const void*>(&attn_naive_kernel),
-                           reinterpret_cast<const void*>(&attn_persistent_kernel)}) {
-      e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kAttnLds);
-      if (e != hipSuccess) return e;
-    }
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&d.per_cu, reinterpret_cast<const void*>(&attn_persistent_kernel),
-                                                     kAttnThreads, kAttnLds);
+                                                     kAttnThreads, 0);
     if (e != hipSuccess) return e;
     if (d.per_cu < 1) d.per_cu = 1;
     cache[dev] = d;
@@ -448,7 +600,7 @@ hipError_t launch_attn(const AttnArgs& a) {
   P.trace = (a.flags & 2u) ? a.trace : nullptr;
 
   if (a.flags & 1u) {
-    hipLaunchKernelGGL(attn_naive_kernel, dim3(n_items), dim3(kAttnThreads), kAttnLds, a.stream, P);
+    hipLaunchKernelGGL(attn_naive_kernel, dim3(n_items), dim3(kAttnThreads), 0, a.stream, P);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, n_items, g.nb, items, counter);
@@ -456,7 +608,7 @@ hipError_t launch_attn(const AttnArgs& a) {
   if (e != hipSuccess) return e;
   int grid = info.cus * info.per_cu;
   if (grid > n_items) grid = n_items;
-  hipLaunchKernelGGL(attn_persistent_kernel, dim3(grid), dim3(kAttnThreads), kAttnLds, a.stream, P, items, n_items,
+  hipLaunchKernelGGL(attn_persistent_kernel, dim3(grid), dim3(kAttnThreads), 0, a.stream, P, items, n_items,
                      counter);
   return hipGetLastError();
 }
