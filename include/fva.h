@@ -32,8 +32,10 @@
  *   written. FVA_ERR_HIP reports a failed kernel launch.
  * - Reentrancy: calls may overlap on different streams if their workspaces
  *   and outputs are distinct.
- * - Supported shapes: head_dim == 128, bt*bh*bw in {64, 128}, nb <= 1024.
- *   Anything else returns FVA_ERR_UNSUPPORTED (there is no slow generic path).
+ * - Supported shapes: head_dim == 128, bt*bh*bw in {64, 128}, nb <= 1024,
+ *   tokens * stride_n * 2 < 2^31 (one head addressed with 32-bit byte
+ *   offsets). Anything else returns FVA_ERR_UNSUPPORTED (there is no slow
+ *   generic path).
  */
 #ifndef FVA_H
 #define FVA_H
@@ -49,7 +51,7 @@ typedef enum fva_status {
   FVA_OK = 0,
   FVA_ERR_INVALID_ARG = -1, /* null pointer, p outside [0,1] or NaN, k_min < 0, bad flags */
   FVA_ERR_SHAPE = -2,       /* tokens != T*H*W, non-positive extents, bad strides */
-  FVA_ERR_UNSUPPORTED = -3, /* head_dim != 128, tile volume not 64/128, nb > 1024 */
+  FVA_ERR_UNSUPPORTED = -3, /* head_dim != 128, tile volume not 64/128, nb > 1024, head > 2 GiB */
   FVA_ERR_WORKSPACE = -4,   /* workspace missing or smaller than the query says */
   FVA_ERR_HIP = -5          /* a kernel launch failed */
 } fva_status;

@@ -13,10 +13,14 @@
 // accumulator of S^T, converted to bf16, is directly the B operand of the PV
 // product (8 consecutive keys per lane) without any register shuffle.
 //
-// Scheduling: a persistent grid pulls items from a list ordered by descending
-// kept-block count (longest-processing-time first) through one atomic
-// counter; FVA_SCHED_NAIVE launches the same item body once per item in
-// head-major order.
+// Scheduling: a persistent grid (2 workgroups per CU) pulls items from one
+// queue per XCD. plan_kernel cuts every head's query blocks into 8 runs of
+// equal kept-block cost, run x into queue x, heads in decreasing cost, so the
+// XCDs stay balanced by construction, work on the same head together (its K/V
+// stay in the shared last-level cache) and the workgroups resident on one XCD
+// work on neighbouring query blocks (their kept K/V overlap in L2). A
+// workgroup whose queue is empty steals from the others. FVA_SCHED_NAIVE
+// launches the same item body once per item in head-major order.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -106,19 +110,32 @@ __device__ __forceinline__ void wait_vmem() {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Row element offsets (relative to the head base) of the 8 LDS rows this
-// lane fills: wave w fills rows 32w .. 32w+31 (key group w), four rows per
-// load instruction. Padding rows repeat the last real row (finite values;
-// their scores are masked).
+// Byte offsets (relative to the head base) of the 8 LDS rows this lane
+// fills: wave w fills rows 32w .. 32w+31 (key group w), four rows per load
+// instruction, so the lane's u-th row holds key
+// kap = 32w + 8(u%4) + 4(u/4) + lane/16. Padding rows repeat the last real
+// row (finite values; their scores are masked).
 __device__ __forceinline__ void row_offsets(const AttnParams& P, const BlockMap& m, int (&roff)[8]) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
+  const int lq = lane >> 4;
+  const int sn2 = 2 * (int)P.sn;  // bytes per token row
+  const int W = P.g.W;
   const int HW = P.g.H * P.g.W;
+  if (m.plane == 64 && m.ex == 8) {
+    // Full 8x8 planes: kap / 64 = w / 2, (kap / 8) % 8 = 4(w % 2) + u % 4,
+    // kap % 8 = 4(u / 4) + lq, and every row is real (n = 64 or 128).
+    const int a = (m.tbase + (w >> 1) * HW + 4 * (w & 1) * W) * sn2;  // wave-uniform
+    const int l = lq * sn2;
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int rho = w * 32 + u * 4 + (lane >> 4);
-    const int kap = min(key_of_row(rho), m.n - 1);
-    roff[u] = row_token(m, kap, HW, P.g.W) * (int)P.sn;
+    for (int u = 0; u < 8; ++u) roff[u] = a + ((u & 3) * W + 4 * (u >> 2)) * sn2 + l;
+  } else {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int rho = w * 32 + u * 4 + lq;
+      const int kap = min(key_of_row(rho), m.n - 1);
+      roff[u] = row_token(m, kap, HW, W) * sn2;
+    }
   }
 }
 
@@ -145,7 +162,7 @@ __device__ __forceinline__ void issue_tile(const uint16_t* __restrict__ src, con
   for (int u = 0; u < 8; ++u) {
     // rho = 32w + 4u + lq, so rho % 16 = 4(u % 4) + lq and rho % 8 = 4(u % 2) + lq
     const int chunk = IS_V ? (p ^ (2 * (4 * (u & 1) + lq))) : (p ^ (4 * (u & 3) + lq));
-    const uint32_t off = (uint32_t)roff[u] * 2u + 16u * (uint32_t)chunk;
+    const uint32_t off = (uint32_t)roff[u] + 16u * (uint32_t)chunk;
     const uint32_t dst = lds0 + (uint32_t)((w * 8 + u) * 1024);
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
                  :
@@ -161,11 +178,31 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 a, f32x4 b) {
 
 __device__ __forceinline__ int ngroups_of(int n) { return (n + 31) >> 5; }
 
+// max / sum over lanes l, l^16, l^32, l^48 (the four lane groups holding one
+// query row) with the gfx950 lane-swap instructions; no LDS traffic.
+__device__ __forceinline__ float row_max4(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float row_sum4(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // Workgroup barrier without a memory fence: the only cross-wave traffic in
 // the block loop is the LDS tiles written by global->LDS copies, and every
 // wave waits for its own copies (vmcnt) before arriving here.
 __device__ __forceinline__ void tile_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// S^T tiles of one 64-key half: LDS tiles 4hb .. 4hb + 2*NGH - 1 against the
+// two 16-row Q tiles. The fragments of tile t+1 load while tile t multiplies
+// (two fragment buffers, renamed at compile time).
 __device__ void process_item(const AttnParams& P, int item, unsigned char* __restrict__ Ks,
                              unsigned char* __restrict__ Vs) {
   const int nb = P.g.nb;
@@ -241,7 +278,6 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
     }
   }
 
-  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
   auto vfrag = [&](int kg, int mt) {
     const unsigned char* vb = Vs + kg * 32 * kRowBytes + vrow + 8 * (4 * (mt ^ vsw) + tq);
     const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds_void*)vb);
@@ -337,15 +373,20 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
             }
           }
         }
+        // The exponent reference mrow only moves when a row's max exceeds it
+        // by more than 2^8 (in exp2 units): P stays <= 256, exact in bf16
+        // scaling, and the O rescale is rare. O and l share the reference, so
+        // the final O / l is unchanged.
         float alpha[2], negm[2];
+        bool grow[2];
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
-          mx[nt] = fmaxf(mx[nt], __shfl_xor(mx[nt], 16));
-          mx[nt] = fmaxf(mx[nt], __shfl_xor(mx[nt], 32));
-          const float mnew = fmaxf(mrow[nt], mx[nt]);
-          negm[nt] = -mnew * P.c2;
-          alpha[nt] = __builtin_amdgcn_exp2f(fmaf(mrow[nt], P.c2, negm[nt]));
-          mrow[nt] = mnew;
+          mx[nt] = row_max4(mx[nt]);
+          grow[nt] = (mx[nt] - mrow[nt]) * P.c2 > 8.0f;
+          const float mref = grow[nt] ? mx[nt] : mrow[nt];
+          alpha[nt] = grow[nt] ? __builtin_amdgcn_exp2f((mrow[nt] - mref) * P.c2) : 1.0f;
+          negm[nt] = -mref * P.c2;
+          mrow[nt] = mref;
         }
         float rs[2] = {0.f, 0.f};
 #pragma unroll
@@ -370,12 +411,8 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         }
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
-          rs[nt] += __shfl_xor(rs[nt], 16);
-          rs[nt] += __shfl_xor(rs[nt], 32);
-          lrow[nt] = lrow[nt] * alpha[nt] + rs[nt];
-          // Once the running max stops moving, alpha == 1 exactly and the
-          // rescale is skipped.
-          if (__ballot(alpha[nt] != 1.0f)) {
+          lrow[nt] = lrow[nt] * alpha[nt] + row_sum4(rs[nt]);
+          if (__ballot(grow[nt])) {
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha[nt];
           }
@@ -453,56 +490,157 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams 
   }
 }
 
+// Persistent scheduler. The work list holds kQueues queues, one per XCD;
+// workgroups pull from the queue of the XCD they run on and steal from the
+// others once theirs is empty.
+constexpr int kQueues = 8;
+
+__device__ __forceinline__ int xcc_id() {
+  uint32_t xcc;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+  return (int)(xcc & 0xfu);
+}
+
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnParams P, const int32_t* __restrict__ items,
-                                                                          int n_items, int32_t* __restrict__ counter) {
+                                                                          const int32_t* __restrict__ qbase,
+                                                                          int32_t* __restrict__ qctr) {
   __shared__ __align__(16) unsigned char ks_tile[kTileBytes];
   __shared__ __align__(16) unsigned char vs_tile[kTileBytes];
-  __shared__ int next;
+  __shared__ int next_slot, next_q;
+  int q = xcc_id() % kQueues;
   for (;;) {
+    if (threadIdx.x == 0) {
+      int slot = -1, qq = q;
+      for (int t = 0; t < kQueues; ++t) {
+        qq = (q + t) % kQueues;
+        const int len = qbase[qq + 1] - qbase[qq];
+        if (len <= 0) continue;
+        const int k = atomicAdd(&qctr[qq], 1);
+        if (k < len) {
+          slot = qbase[qq] + k;
+          break;
+        }
+      }
+      next_slot = slot;
+      next_q = qq;
+    }
     __syncthreads();
-    if (threadIdx.x == 0) next = atomicAdd(counter, 1);
-    __syncthreads();
-    const int slot = __builtin_amdgcn_readfirstlane(next);
-    if (slot >= n_items) break;
+    const int slot = __builtin_amdgcn_readfirstlane(next_slot);
+    q = __builtin_amdgcn_readfirstlane(next_q);  // keep stealing from a queue that had work
+    if (slot < 0) break;
     const int item = __builtin_amdgcn_readfirstlane(items[slot]);
     const int64_t t0 = (int64_t)wall_clock64();
     process_item(P, item, ks_tile, vs_tile);
-    __syncthreads();  // the next item's copies overwrite the tiles
-    if (P.trace) {
-      __syncthreads();
-      trace_item(P, item, t0);
-    }
+    __syncthreads();  // the next item's copies overwrite the tiles; next_slot is rewritten
+    if (P.trace) trace_item(P, item, t0);
   }
 }
 
-// Longest-processing-time order: items sorted by kept-block count, largest
-// first (counting sort in one workgroup); also resets the queue counter.
-__global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ counts, int n_items, int nb,
-                                                   int32_t* __restrict__ items, int32_t* __restrict__ counter) {
-  __shared__ int hist[kMaxBlocks + 1];
-  for (int c = threadIdx.x; c <= nb; c += blockDim.x) hist[c] = 0;
+// Builds the per-XCD queues (one workgroup). Heads are taken in decreasing
+// order of cost (sum over rows of kept blocks + 1). Each head's query blocks
+// are cut into kQueues contiguous runs of about equal cost, run x going to
+// queue x, so all XCDs work on the same head at the same time (its K/V stay
+// in the shared last-level cache) and the resident workgroups of one XCD
+// work on neighbouring query blocks (their kept K/V blocks overlap in L2).
+// Scratch per head: cost, rank, run starts [kQueues + 1], queue offsets [kQueues].
+__global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ counts, int n_heads, int nb,
+                                                   int32_t* __restrict__ items, int32_t* __restrict__ qbase,
+                                                   int32_t* __restrict__ qctr, int32_t* __restrict__ hscratch) {
+  int32_t* hcost = hscratch;
+  int32_t* horder = hcost + n_heads;
+  int32_t* hstart = horder + n_heads;                  // [n_heads][kQueues + 1]
+  int32_t* hoff = hstart + (size_t)n_heads * (kQueues + 1);  // [n_heads][kQueues]
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  auto cost_of = [&](int h, int i) {
+    const int c = counts[(int64_t)h * nb + i];
+    return (c < 0 ? 0 : (c > nb ? nb : c)) + 1;
+  };
+
+  // 1. head costs and equal-cost runs (one wave per head)
+  for (int h = wave; h < n_heads; h += nwaves) {
+    int total = 0;
+    for (int i0 = 0; i0 < nb; i0 += 64) total += (i0 + lane < nb) ? cost_of(h, i0 + lane) : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) total += __shfl_xor(total, o);
+    if (lane == 0) hcost[h] = total;
+    // run of row i = floor(kQueues * (cost before row i) / total), a
+    // non-decreasing function of i; run x starts at the first row whose run
+    // is >= x (nb when there is none).
+    int stx[kQueues + 1];
+#pragma unroll
+    for (int x = 0; x <= kQueues; ++x) stx[x] = nb;
+    int run_before = 0;
+    for (int i0 = 0; i0 < nb; i0 += 64) {
+      const int i = i0 + lane;
+      const int c = i < nb ? cost_of(h, i) : 0;
+      const int incl = wave_incl_scan_i32(c, lane);
+      const int before = run_before + incl - c;
+      const int run = (int)(((int64_t)before * kQueues) / total);
+#pragma unroll
+      for (int x = 0; x < kQueues; ++x) {
+        const uint64_t hit = __ballot(i < nb && run >= x);
+        if (stx[x] == nb && hit) stx[x] = i0 + __ffsll((unsigned long long)hit) - 1;
+      }
+      run_before += __shfl(incl, 63);
+    }
+    int32_t* st = hstart + (size_t)h * (kQueues + 1);
+    if (lane == 0) {
+#pragma unroll
+      for (int x = 0; x <= kQueues; ++x) st[x] = stx[x];
+    }
+  }
   __syncthreads();
-  for (int r = threadIdx.x; r < n_items; r += blockDim.x) {
-    int c = counts[r];
-    c = c < 0 ? 0 : (c > nb ? nb : c);
-    atomicAdd(&hist[c], 1);
+
+  // 2. head order by decreasing cost (ties: lower head first)
+  for (int h = threadIdx.x; h < n_heads; h += blockDim.x) {
+    const int ch = hcost[h];
+    int rank = 0;
+    for (int k = 0; k < n_heads; ++k) {
+      const int ck = hcost[k];
+      rank += (ck > ch || (ck == ch && k < h)) ? 1 : 0;
+    }
+    horder[rank] = h;
+  }
+  __syncthreads();
+
+  // 3. queue offsets of every (head, run) and queue bases
+  if (threadIdx.x < kQueues) {
+    const int x = threadIdx.x;
+    int run = 0;
+    for (int r = 0; r < n_heads; ++r) {
+      const int h = horder[r];
+      const int32_t* st = hstart + (size_t)h * (kQueues + 1);
+      hoff[(size_t)h * kQueues + x] = run;
+      run += st[x + 1] - st[x];
+    }
+    qctr[x] = run;  // queue length for now
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    int run = 0;
-    for (int c = nb; c >= 0; --c) {
-      const int n = hist[c];
-      hist[c] = run;
-      run += n;
+    int base = 0;
+    for (int x = 0; x < kQueues; ++x) {
+      const int len = qctr[x];
+      qbase[x] = base;
+      base += len;
     }
-    *counter = 0;
+    qbase[kQueues] = base;
   }
   __syncthreads();
+
+  // 4. scatter items into their queues, reset the queue counters
+  const int n_items = n_heads * nb;
   for (int r = threadIdx.x; r < n_items; r += blockDim.x) {
-    int c = counts[r];
-    c = c < 0 ? 0 : (c > nb ? nb : c);
-    items[atomicAdd(&hist[c], 1)] = r;
+    const int h = r / nb;
+    const int i = r - h * nb;
+    const int32_t* st = hstart + (size_t)h * (kQueues + 1);
+    int x = 0;
+    while (x + 1 < kQueues && st[x + 1] <= i) ++x;
+    items[qbase[x] + hoff[(size_t)h * kQueues + x] + (i - st[x])] = r;
   }
+  __syncthreads();
+  if (threadIdx.x < kQueues) qctr[threadIdx.x] = 0;
 }
 
 // counts and ascending kept-block lists from a block mask, one wave per row.
@@ -551,24 +689,51 @@ hipError_t device_info(DeviceInfo& info) {
 
 }  // namespace
 
-size_t attn_workspace_bytes(int batch, int heads, int nb) {
+namespace {
+struct AttnWorkspace {
+  int32_t* counts;   // [rows]        rebuilt counts (caller passed none)
+  int32_t* kv;       // [rows][nb]    rebuilt kept lists
+  int32_t* items;    // [rows]        queue contents
+  int32_t* qbase;    // [kQueues + 1]
+  int32_t* qctr;     // [kQueues]
+  int32_t* hscratch; // [heads * (2 + 2 * kQueues + 1)]
+  size_t bytes;
+};
+
+AttnWorkspace carve(void* base, int batch, int heads, int nb) {
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t rows = (size_t)batch * heads * nb;
-  return al(rows * 4) + al(rows * nb * 4) + al(rows * 4) + al(4);
+  const size_t nh = (size_t)batch * heads;
+  char* p = reinterpret_cast<char*>(base);
+  AttnWorkspace w;
+  size_t off = 0;
+  w.counts = reinterpret_cast<int32_t*>(p + off);
+  off += al(rows * 4);
+  w.kv = reinterpret_cast<int32_t*>(p + off);
+  off += al(rows * nb * 4);
+  w.items = reinterpret_cast<int32_t*>(p + off);
+  off += al(rows * 4);
+  w.qbase = reinterpret_cast<int32_t*>(p + off);
+  off += al((kQueues + 1) * 4);
+  w.qctr = reinterpret_cast<int32_t*>(p + off);
+  off += al(kQueues * 4);
+  w.hscratch = reinterpret_cast<int32_t*>(p + off);
+  off += al(nh * (2 + 2 * kQueues + 1) * 4);
+  w.bytes = off;
+  return w;
 }
+}  // namespace
+
+size_t attn_workspace_bytes(int batch, int heads, int nb) { return carve(nullptr, batch, heads, nb).bytes; }
 
 hipError_t launch_attn(const AttnArgs& a) {
   (void)hipGetLastError();  // drop an error left by an unrelated earlier HIP call
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
   const int n_items = a.batch * a.heads * g.nb;
   if (n_items == 0) return hipSuccess;
-  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  char* ws = reinterpret_cast<char*>(a.workspace);
-  int32_t* ws_counts = reinterpret_cast<int32_t*>(ws);
-  int32_t* ws_kv = reinterpret_cast<int32_t*>(ws + al((size_t)n_items * 4));
-  int32_t* items = reinterpret_cast<int32_t*>(ws + al((size_t)n_items * 4) + al((size_t)n_items * g.nb * 4));
-  int32_t* counter = items + (al((size_t)n_items * 4) / 4);
-
+  const AttnWorkspace ws = carve(a.workspace, a.batch, a.heads, g.nb);
+  int32_t* ws_counts = ws.counts;
+  int32_t* ws_kv = ws.kv;
   DeviceInfo info;
   hipError_t e = device_info(info);
   if (e != hipSuccess) return e;
@@ -603,13 +768,14 @@ hipError_t launch_attn(const AttnArgs& a) {
     hipLaunchKernelGGL(attn_naive_kernel, dim3(n_items), dim3(kAttnThreads), 0, a.stream, P);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, n_items, g.nb, items, counter);
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, a.batch * a.heads, g.nb, ws.items,
+                     ws.qbase, ws.qctr, ws.hscratch);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   int grid = info.cus * info.per_cu;
   if (grid > n_items) grid = n_items;
-  hipLaunchKernelGGL(attn_persistent_kernel, dim3(grid), dim3(kAttnThreads), 0, a.stream, P, items, n_items,
-                     counter);
+  hipLaunchKernelGGL(attn_persistent_kernel, dim3(grid), dim3(kAttnThreads), 0, a.stream, P, ws.items, ws.qbase,
+                     ws.qctr);
   return hipGetLastError();
 }
 

@@ -30,6 +30,8 @@ fva_status check_shape(const fva_qkv_desc* d, const fva_tiling* t, int* nb_out) 
   // Strides are in elements; every token row must start on a 16-byte boundary.
   if (d->stride_n < d->head_dim || d->stride_h < 0 || d->stride_b < 0) return FVA_ERR_SHAPE;
   if (d->stride_n % 8 != 0 || d->stride_h % 8 != 0 || d->stride_b % 8 != 0) return FVA_ERR_SHAPE;
+  // Kernels address a head with 32-bit byte offsets.
+  if ((int64_t)d->tokens * d->stride_n * 2 >= ((int64_t)1 << 31)) return FVA_ERR_UNSUPPORTED;
   *nb_out = g.nb;
   return FVA_OK;
 }

@@ -55,7 +55,10 @@ def test_workspace_sizes():
     rows = 40 * nb
     assert fva.fva_route_workspace_size(desc(), T720) == 2 * rows * 128 * 8
     al = lambda x: (x + 255) // 256 * 256
-    assert fva.fva_attn_workspace_size(desc(), T720) == al(rows * 4) + al(rows * nb * 4) + al(rows * 4) + al(4)
+    # counts, kept lists, queue items, 9 queue bases, 8 queue counters, per-head plan scratch
+    heads = 40
+    expect = al(rows * 4) + al(rows * nb * 4) + al(rows * 4) + al(9 * 4) + al(8 * 4) + al(heads * 19 * 4)
+    assert fva.fva_attn_workspace_size(desc(), T720) == expect
     assert fva.fva_trace_words(desc(), T720) == rows * 4
 
 
