@@ -49,12 +49,19 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
   const int c = threadIdx.x & 15;    // 16-byte chunk: dims 8c .. 8c+7
   const int slot = threadIdx.x >> 4;  // token slot 0..15
 
+  // Row r = slot + 16u of the block. For full 8x8 planes, r / 64, (r / 8) % 8
+  // and r % 8 are (u / 4, 2(u % 4) + slot / 8, slot % 8): no divisions.
+  const bool fast = box.ey == 8 && box.ex == 8;
+  const int HW = g.H * g.W;
+  const int tb = (box.t0 * g.H + box.y0) * g.W + box.x0;
+  const int lane_tok = (slot >> 3) * g.W + (slot & 7);
   uint4 vq[8], vk[8];
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     const int r = slot + 16 * u;
     if (r < box.n) {
-      const int64_t off = base + (int64_t)box_token(g, box, r) * sn + c * 8;
+      const int tok = fast ? tb + (u >> 2) * HW + 2 * (u & 3) * g.W + lane_tok : box_token(g, box, r);
+      const int64_t off = base + (int64_t)tok * sn + c * 8;
       vq[u] = *reinterpret_cast<const uint4*>(Q + off);
       vk[u] = *reinterpret_cast<const uint4*>(K + off);
     } else {
@@ -92,10 +99,11 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
   out[((int64_t)bh * g.nb + i) * kHeadDim + d] = s / (double)box.n;
 }
 
-// Fixed-point mass of one block: round(exp(s - smax) / Z * 2^62).
-__device__ __forceinline__ uint64_t block_mass(double s, double smax, double Z) {
-  const double P = __ddiv_rn(exp(s - smax), Z);
-  return (uint64_t)__double2ull_rn(__dmul_rn(P, kMassScale));
+// Fixed-point mass of one block: round(exp(s - smax) * (2^62 / Z)). Every
+// caller evaluates exactly this expression, so a block's mass is the same
+// wherever it is recomputed.
+__device__ __forceinline__ uint64_t block_mass(double s, double smax, double zs) {
+  return (uint64_t)__double2ull_rn(__dmul_rn(exp(s - smax), zs));
 }
 
 struct WaveScratch {
@@ -117,7 +125,7 @@ struct Cut {
 // (score desc, id asc) order. Requires thr >= 1 and total weight >= thr.
 template <int KPL>
 __device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL], const uint64_t (&F)[KPL],
-                          uint32_t valid, double smin, double smax, double Z, bool by_mass, uint64_t thr,
+                          uint32_t valid, double smin, double smax, double zs, bool by_mass, uint64_t thr,
                           WaveScratch& ws, int lane) {
   uint32_t cand = valid;
   uint64_t W0 = 0;
@@ -144,7 +152,7 @@ __device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL
       if (!(hi > lo) && ncand > 64) {
         // Every candidate has the same score: they follow in id order, each
         // with the same weight, so the cut is the t-th smallest id.
-        const uint64_t w = by_mass ? block_mass(hi, smax, Z) : 1ull;
+        const uint64_t w = by_mass ? block_mass(hi, smax, zs) : 1ull;
         const uint64_t need = thr - W0;
         uint64_t t = (w == 0) ? (uint64_t)ncand : (need + w - 1) / w;
         if (t > (uint64_t)ncand) t = (uint64_t)ncand;
@@ -180,7 +188,7 @@ __device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL
         const double sm = srow[jm];
         rank += (sm > sl || (sm == sl && jm < jl)) ? 1 : 0;
       }
-      const uint64_t wl = has ? (by_mass ? block_mass(sl, smax, Z) : 1ull) : 0ull;
+      const uint64_t wl = has ? (by_mass ? block_mass(sl, smax, zs) : 1ull) : 0ull;
       wave_sync();
       if (has && rank < 64) {
         ws.slot_j[rank] = jl;
@@ -198,15 +206,16 @@ __device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL
       wave_sync();
       return c;
     }
-    // Bucket the candidates by score, highest scores in bucket 0.
+    // Bucket the candidates by score, highest scores in bucket 0: the bucket
+    // floor((hi - s) * 64 / (hi - lo)) is non-decreasing as s falls.
     ws.cnt[lane] = 0u;
     ws.wt[lane] = 0ull;
     wave_sync();
-    const double span = hi - lo;
+    const double scale = __ddiv_rn(64.0, hi - lo);
 #pragma unroll
     for (int k = 0; k < KPL; ++k) {
       if ((cand >> k) & 1u) {
-        int bkt = (int)(64.0 * __ddiv_rn(hi - s[k], span));
+        int bkt = (int)__dmul_rn(hi - s[k], scale);
         bkt = bkt < 0 ? 0 : (bkt > 63 ? 63 : bkt);
         atomicAdd(&ws.cnt[bkt], 1u);
         atomicAdd((unsigned long long*)&ws.wt[bkt], (unsigned long long)(by_mass ? F[k] : 1ull));
@@ -226,7 +235,7 @@ __device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL
 #pragma unroll
     for (int k = 0; k < KPL; ++k) {
       if ((cand >> k) & 1u) {
-        int bkt = (int)(64.0 * __ddiv_rn(hi - s[k], span));
+        int bkt = (int)__dmul_rn(hi - s[k], scale);
         bkt = bkt < 0 ? 0 : (bkt > 63 ? 63 : bkt);
         if (bkt != bstar) {
           cand &= ~(1u << k);
@@ -274,10 +283,11 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
   for (int k = 0; k < KPL; ++k)
     if ((valid >> k) & 1u) e += exp(s[k] - smax);
   const double Z = wave_sum(e);
+  const double zs = __ddiv_rn(kMassScale, Z);
   uint64_t tot = 0;
 #pragma unroll
   for (int k = 0; k < KPL; ++k) {
-    F[k] = ((valid >> k) & 1u) ? block_mass(s[k], smax, Z) : 0ull;
+    F[k] = ((valid >> k) & 1u) ? block_mass(s[k], smax, zs) : 0ull;
     tot += F[k];
   }
   const uint64_t total = wave_sum_u64(tot);
@@ -297,12 +307,12 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
     } else if (total < T) {
       m_p = nb;
     } else {
-      cut = select_cut<KPL>(srow, s, F, valid, smin, smax, Z, true, T, ws, lane);
+      cut = select_cut<KPL>(srow, s, F, valid, smin, smax, zs, true, T, ws, lane);
       m_p = cut.rank;
     }
   }
   const int m = m_p > kf ? m_p : kf;
-  if (m > 0 && m < nb && m != m_p) cut = select_cut<KPL>(srow, s, F, valid, smin, smax, Z, false, (uint64_t)m, ws, lane);
+  if (m > 0 && m < nb && m != m_p) cut = select_cut<KPL>(srow, s, F, valid, smin, smax, zs, false, (uint64_t)m, ws, lane);
 
   int base = 0;
 #pragma unroll
@@ -321,44 +331,68 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
   if (lane == 0) *count_out = m;
 }
 
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+constexpr int kSelThreads = 512;  // 8 waves
+
+// Scores of 16 query blocks against every key block with the fp64 MFMA
+// (16x16x4): lane (row l%16, group g = l/16) feeds q_row[32g + ks] and
+// k_key[32g + ks] at step ks, so each lane reads 256 contiguous bytes per
+// operand and the 32 steps sum the full 128-dim dot product. Wave w takes key
+// tiles w, w+8, ...; then each wave selects rows w and w+8.
 template <int KPL>
-__global__ __launch_bounds__(1024) void select_kernel(const double* __restrict__ qbar,
-                                                     const double* __restrict__ kbar, int nb, double p, int k_min,
-                                                     uint8_t* __restrict__ mask, int32_t* __restrict__ counts,
-                                                     int32_t* __restrict__ kv_idx) {
+__global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __restrict__ qbar,
+                                                                const double* __restrict__ kbar, int nb, double p,
+                                                                int k_min, uint8_t* __restrict__ mask,
+                                                                int32_t* __restrict__ counts,
+                                                                int32_t* __restrict__ kv_idx) {
   extern __shared__ __align__(16) unsigned char smem[];
   double* sc = reinterpret_cast<double*>(smem);  // [kSelRows][nb]
   WaveScratch* wsa = reinterpret_cast<WaveScratch*>(smem + sizeof(double) * kSelRows * nb);
   const int bh = blockIdx.y;
   const int i0 = blockIdx.x * kSelRows;
   const int rows = min(kSelRows, nb - i0);
-  const double* qb = qbar + ((int64_t)bh * nb + i0) * kHeadDim;
-  const double* kb = kbar + (int64_t)bh * nb * kHeadDim;
-  const double inv_scale = 11.313708498984761;  // sqrt(128)
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nwaves = kSelThreads / 64;
+  const int m16 = lane & 15;
+  const int g = lane >> 4;
+  const double inv_sqrt_d = 11.313708498984761;  // sqrt(128): s = dot / sqrt(128)
 
-  // Scores: one thread per key block, all rows of the workgroup at once.
-  for (int j = threadIdx.x; j < nb; j += blockDim.x) {
-    double acc[kSelRows];
+  // A operand: q of row min(m16, rows-1), dims 32g .. 32g+31
+  double qa[32];
+  {
+    const double* qr = qbar + ((int64_t)bh * nb + i0 + min(m16, rows - 1)) * kHeadDim + 32 * g;
 #pragma unroll
-    for (int r = 0; r < kSelRows; ++r) acc[r] = 0.0;
-    const double* kr = kb + (int64_t)j * kHeadDim;
-    for (int d = 0; d < kHeadDim; d += 2) {
-      const double2 kv = *reinterpret_cast<const double2*>(kr + d);
-#pragma unroll
-      for (int r = 0; r < kSelRows; ++r) {
-        const int rr = r < rows ? r : rows - 1;
-        acc[r] = fma(qb[rr * kHeadDim + d], kv.x, acc[r]);
-        acc[r] = fma(qb[rr * kHeadDim + d + 1], kv.y, acc[r]);
-      }
+    for (int k = 0; k < 32; k += 2) {
+      const double2 v = *reinterpret_cast<const double2*>(qr + k);
+      qa[k] = v.x;
+      qa[k + 1] = v.y;
     }
+  }
+  const int ntiles = (nb + 15) >> 4;
+  const double* kb = kbar + (int64_t)bh * nb * kHeadDim;
+  for (int t = wave; t < ntiles; t += nwaves) {
+    const int key = t * 16 + m16;
+    const double* kr = kb + (int64_t)min(key, nb - 1) * kHeadDim + 32 * g;
+    double kk[32];
 #pragma unroll
-    for (int r = 0; r < kSelRows; ++r) sc[r * nb + j] = __ddiv_rn(acc[r], inv_scale);
+    for (int k = 0; k < 32; k += 2) {
+      const double2 v = *reinterpret_cast<const double2*>(kr + k);
+      kk[k] = v.x;
+      kk[k + 1] = v.y;
+    }
+    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int k = 0; k < 32; ++k) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[k], kk[k], acc, 0, 0, 0);
+    // D layout of the fp64 16x16x4 MFMA: lane holds rows g + 4e (e = 0..3)
+    // of key column m16.
+    if (key < nb) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sc[(g + 4 * e) * nb + key] = __ddiv_rn(acc[e], inv_sqrt_d);
+    }
   }
   __syncthreads();
 
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int nwaves = blockDim.x >> 6;
   for (int r = wave; r < rows; r += nwaves) {
     const int64_t row = (int64_t)bh * nb + i0 + r;
     select_row<KPL>(sc + r * nb, nb, p, k_min, mask + row * nb, counts + row, kv_idx ? kv_idx + row * nb : nullptr,
@@ -369,9 +403,7 @@ __global__ __launch_bounds__(1024) void select_kernel(const double* __restrict__
 template <int KPL>
 hipError_t launch_select(const RouteArgs& a, int nb, double* qbar, double* kbar) {
   const int bhs = a.batch * a.heads;
-  int threads = ((nb + 63) / 64) * 64;
-  if (threads > 1024) threads = 1024;
-  const size_t lds = sizeof(double) * kSelRows * nb + sizeof(WaveScratch) * (threads / 64);
+  const size_t lds = sizeof(double) * kSelRows * nb + sizeof(WaveScratch) * (kSelThreads / 64);
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<KPL>),
@@ -380,7 +412,7 @@ hipError_t launch_select(const RouteArgs& a, int nb, double* qbar, double* kbar)
     attr_set = true;
   }
   dim3 grid((nb + kSelRows - 1) / kSelRows, bhs);
-  hipLaunchKernelGGL(select_kernel<KPL>, grid, dim3(threads), lds, a.stream, qbar, kbar, nb, a.p, a.k_min, a.mask,
+  hipLaunchKernelGGL(select_kernel<KPL>, grid, dim3(kSelThreads), lds, a.stream, qbar, kbar, nb, a.p, a.k_min, a.mask,
                      a.counts, a.kv_idx);
   return hipGetLastError();
 }
@@ -410,6 +442,7 @@ hipError_t launch_route(const RouteArgs& a) {
   if (kpl <= 2) return launch_select<2>(a, g.nb, qbar, kbar);
   if (kpl <= 4) return launch_select<4>(a, g.nb, qbar, kbar);
   if (kpl <= 8) return launch_select<8>(a, g.nb, qbar, kbar);
+  if (kpl <= 12) return launch_select<12>(a, g.nb, qbar, kbar);
   return launch_select<16>(a, g.nb, qbar, kbar);
 }
 
