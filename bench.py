@@ -17,6 +17,7 @@ CPU oracle timed on a bounded sample.
 """
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -37,19 +38,64 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def real_pairs(mask, geo):
+def block_sizes(grid, tile):
+    """Real tokens of every block, raster block order (boxes anchored at the origin)."""
+    ext = []
+    for S, b in zip(grid, tile):
+        n = -(-S // b)
+        e = np.full(n, b, dtype=np.int64)
+        e[-1] = S - b * (n - 1)
+        ext.append(e)
+    return np.einsum("a,b,c->abc", *ext).reshape(-1)
+
+
+def real_pairs(mask, sizes):
     """sum over kept (h, i, j) of n_i * n_j (real token pairs)."""
-    n = geo.block_sizes.astype(np.float64)
-    m = mask.reshape(-1, geo.nb, geo.nb).astype(np.float64)
+    n = sizes.astype(np.float64)
+    nb = n.shape[0]
+    m = mask.reshape(-1, nb, nb).astype(np.float64)
     return float(np.einsum("hij,i,j->", m, n, n))
 
 
-def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, geo, budget_s=20.0):
+def source_digest(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def imbalance(trace, counts):
+    """Per-CU and per-XCD load figures from an FVA_TRACE record.
+
+    CU = (xcc, bits 8.. of HW_ID); busy = sum of item durations on the CU.
+    rho = max/mean over XCDs of summed kept blocks (Eq. 2 with XCDs as ranks)
+    and of summed item time.
+    """
+    tr = trace.reshape(-1, 4)
+    dur = (tr[:, 1] - tr[:, 0]).astype(np.float64)
+    loc = tr[:, 2]
+    cu = loc >> 8
+    xcc = loc >> 16
+    cost = counts.reshape(-1).astype(np.float64)
+    _, inv = np.unique(cu, return_inverse=True)
+    busy = np.bincount(inv, weights=dur)
+    xb = np.bincount(xcc, weights=dur, minlength=8)
+    xc = np.bincount(xcc, weights=cost, minlength=8)
+    span = float(tr[:, 1].max() - tr[:, 0].min()) / 100.0  # 100 MHz clock -> us
+    return {
+        "cus_used": int(busy.size),
+        "cu_busy_max_over_mean": round(float(busy.max() / busy.mean()), 4),
+        "xcd_time_rho": round(float(xb.max() / xb.mean()), 4),
+        "xcd_blocks_rho": round(float(xc.max() / xc.mean()), 4),
+        "span_us": round(span, 1),
+    }
+
+
+def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0):
     """Oracle timed on this host on a bounded sample; returns dict."""
-    from oracle import attn_ref_rows, route_ref
+    from oracle import attn_ref_rows, route_ref, tile_geometry
 
     import synth
 
+    geo = tile_geometry(*cfg.grid, *cfg.tile)
     cores = len(os.sched_getaffinity(0))
     f64 = lambda b: synth.bf16_bits_to_f32(b).astype(np.float64)
     H = cfg.heads
@@ -77,7 +123,7 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, geo, budget_s=20.0):
             t_att += time.perf_counter() - t0
             done_pairs += n[i] * float((mask[0, h, i].astype(np.float64) * n).sum())
             rows += 1
-    total_pairs = real_pairs(mask, geo)
+    total_pairs = real_pairs(mask, geo.block_sizes)
     t_att_full = t_att * total_pairs / max(done_pairs, 1.0)
     t_full = t_route + t_att_full
     dense_flops = 4.0 * H * float(geo.N) ** 2 * 128
@@ -93,6 +139,32 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, geo, budget_s=20.0):
     }
 
 
+# HBM bytes per launch of attn_persistent_kernel on the 720p workload from
+# rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each scaled by the factor the same
+# counter reads for a device copy of known size; valid only for the attention
+# source with this digest (null otherwise).
+ATTN_TRAFFIC = {"source_digest": "14e1ab749cf0a865", "workload": "720p", "bytes": 211091655680 + 775206000}
+
+
+def copy_calibration(torch, gib=1.0, reps=5):
+    """Plain device copy of known size (reads and writes `gib` GiB each)."""
+    n = int(gib * (1 << 30))
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(reps):
+        dst.copy_(src)
+    ev[1].record()
+    torch.cuda.synchronize()
+    t = ev[0].elapsed_time(ev[1]) / reps / 1e3
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "copy_s": t,
+                      "copy_GBps_read_plus_write": 2 * n / t / 1e9}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -100,9 +172,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="720p")
     ap.add_argument("--p", type=float, default=None)
+    ap.add_argument("--p-sweep", default=None, help="comma-separated p values, timed after the main run")
     ap.add_argument("--sched", choices=["persistent", "naive"], default="persistent")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-trace", action="store_true", help="skip the scheduler imbalance trace runs")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--copy-calibration", action="store_true", help="only time a 1 GiB device copy")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -115,21 +190,25 @@ def main():
 
     import torch
 
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
+
     import paper_2607_16190_amd as fva
     import synth
-    from oracle.tiling import tile_geometry  # geometry tables for the work counts only
 
     cfg = synth.get_config(args.workload)
     p = cfg.p if args.p is None else args.p
-    geo = tile_geometry(*cfg.grid, *cfg.tile)
     tiling = fva.Tiling(*cfg.grid, *cfg.tile)
+    sizes = block_sizes(cfg.grid, cfg.tile)
     dev = torch.device("cuda:0")
     log(f"[bench] generating {cfg.name}: {cfg.heads} heads x {cfg.N} tokens x 128")
     Qb, Kb, Vb = synth.gen_qkv(cfg)
     up = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
     q, k, v = up(Qb), up(Kb), up(Vb)
     desc = fva._desc_of(q)
-    nb = geo.nb
+    nb = fva.fva_num_blocks(tiling)
+    assert nb == sizes.shape[0]
     B, H = q.shape[0], q.shape[1]
     mask = torch.empty((B, H, nb, nb), dtype=torch.uint8, device=dev)
     counts = torch.empty((B, H, nb), dtype=torch.int32, device=dev)
@@ -140,45 +219,49 @@ def main():
     flags = fva.FVA_SCHED_NAIVE if args.sched == "naive" else fva.FVA_SCHED_PERSISTENT
     stream = torch.cuda.current_stream()
 
-    def step(ev=None):
+    def step(pp, ev=None):
         if ev:
             ev[0].record(stream)
-        fva.fva_route(q, k, p, cfg.k_min, tiling, out=(mask, counts, kv), workspace=ws_r)
+        fva.fva_route(q, k, pp, cfg.k_min, tiling, out=(mask, counts, kv), workspace=ws_r)
         if ev:
             ev[1].record(stream)
         fva.fva_attn(q, k, v, tiling, mask, counts, kv, flags=flags, out=out, workspace=ws_a)
         if ev:
             ev[2].record(stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    log(f"[bench] warmup done ({args.warmup} steps)")
+    def timed(pp, steps, warmup):
+        for _ in range(warmup):
+            step(pp)
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s_ in range(steps):
+            step(pp, evs[s_])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        route_ms = [e[0].elapsed_time(e[1]) for e in evs]
+        attn_ms = [e[1].elapsed_time(e[2]) for e in evs]
+        return wall * 1e3 / steps, float(np.mean(route_ms)) / 1e3, float(np.mean(attn_ms)) / 1e3
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(evs[s])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    route_ms = [e[0].elapsed_time(e[1]) for e in evs]
-    attn_ms = [e[1].elapsed_time(e[2]) for e in evs]
-    ms_per_step = wall * 1e3 / args.steps
-    log(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step (route {np.mean(route_ms)*1e3:.1f} us, "
-        f"attn {np.mean(attn_ms):.3f} ms)")
+    ms_per_step, t_route, t_attn = timed(p, args.steps, args.warmup)
+    log(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step (route {t_route*1e6:.1f} us, "
+        f"attn {t_attn*1e3:.3f} ms)")
 
     m_np = mask.cpu().numpy()
     c_np = counts.cpu().numpy()
     kept = int(c_np.sum())
     d = 128
     N = cfg.N
-    t_attn = float(np.mean(attn_ms)) / 1e3
-    t_route = float(np.mean(route_ms)) / 1e3
     kept_tile_flops = 4.0 * 128 * 128 * d * kept
-    useful_flops = 4.0 * d * real_pairs(m_np, geo)
+    useful_flops = 4.0 * d * real_pairs(m_np, sizes)
     dense_flops = 4.0 * B * H * float(N) ** 2 * d
     route_bytes = 2.0 * B * H * N * d * 2 + B * H * nb * nb + 4.0 * B * H * nb + 4.0 * kept
+    here = os.path.dirname(os.path.abspath(__file__))
+    digest = source_digest(os.path.join(here, "paper_2607_16190_amd", "csrc", "attn_kernels.hip"))
+    traffic = None
+    if ATTN_TRAFFIC["source_digest"] == digest and ATTN_TRAFFIC["workload"] == cfg.name and args.sched == "persistent":
+        traffic = ATTN_TRAFFIC["bytes"]
     res = {
         "metric": METRIC,
         "value": round(dense_flops / (ms_per_step / 1e3) / 1e12, 2),
@@ -218,14 +301,37 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(useful_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
-            "kernel": "attn_persistent_kernel (fva_attn; includes the one-workgroup plan kernel)",
+            "traffic": traffic,
+            "kernel": "attn_persistent_kernel (fva_attn; timed with its plan_kernel)",
             "algorithmic_flops_per_launch": useful_flops,
+            "attn_source_digest": digest,
         },
     }
+    if not args.no_trace:
+        tw = fva.fva_trace_words(desc, tiling)
+        trace = torch.zeros(tw, dtype=torch.int64, device=dev)
+        imb = {}
+        for name, fl in (("persistent", fva.FVA_SCHED_PERSISTENT), ("naive", fva.FVA_SCHED_NAIVE)):
+            trace.zero_()
+            fva.fva_attn(q, k, v, tiling, mask, counts, kv, flags=fl | fva.FVA_TRACE, out=out, workspace=ws_a,
+                         trace=trace)
+            torch.cuda.synchronize()
+            imb[name] = imbalance(trace.cpu().numpy(), c_np)
+        res["scheduler_trace"] = imb
+        log(f"[bench] trace: {imb}")
+    if args.p_sweep:
+        sweep = []
+        for pp in [float(x) for x in args.p_sweep.split(",")]:
+            msp, tr_, ta_ = timed(pp, max(2, args.steps // 2), 1)
+            cc = counts.cpu().numpy()
+            sweep.append({"p": pp, "retained_fraction": round(float(cc.sum()) / (B * H * nb * nb), 4),
+                          "ms_per_step": round(msp, 3), "route_us": round(tr_ * 1e6, 1),
+                          "attn_ms": round(ta_ * 1e3, 3)})
+            log(f"[bench] p={pp}: {sweep[-1]}")
+        res["p_sweep"] = sweep
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
-        res["cpu_baseline"] = cpu_baseline(cfg, Qb, Kb, Vb, m_np, c_np, geo, args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(cfg, Qb, Kb, Vb, m_np, c_np, args.cpu_budget)
     print(json.dumps(res), flush=True)
 
 

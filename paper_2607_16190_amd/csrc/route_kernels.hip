@@ -178,14 +178,16 @@ __device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL
         c.rank = C0 + (int)t;
         return c;
       }
-      // At most 64 candidates: rank them exactly.
+      // At most 64 candidates: rank them exactly. Candidate m's score and
+      // id are broadcast from lane m with readlane (no memory round trips).
       const bool has = lane < ncand;
       const int jl = has ? ws.list_j[lane] : 0;
-      double sl = srow[jl];
+      const double sl = srow[jl];
       int rank = 0;
       for (int m = 0; m < ncand; ++m) {  // ncand <= 64 here
-        const int jm = ws.list_j[m];
-        const double sm = srow[jm];
+        const int jm = __builtin_amdgcn_readlane(jl, m);
+        const double sm = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(sl), m),
+                                           __builtin_amdgcn_readlane(__double2loint(sl), m));
         rank += (sm > sl || (sm == sl && jm < jl)) ? 1 : 0;
       }
       const uint64_t wl = has ? (by_mass ? block_mass(sl, smax, zs) : 1ull) : 0ull;
@@ -278,16 +280,21 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
   }
   const double smax = wave_max(vmax);
   const double smin = wave_min(vmin);
+  // F[k] first holds exp(s - smax) (as bits), then the fixed-point mass;
+  // block_mass evaluates the same two roundings.
   double e = 0.0;
 #pragma unroll
-  for (int k = 0; k < KPL; ++k)
-    if ((valid >> k) & 1u) e += exp(s[k] - smax);
+  for (int k = 0; k < KPL; ++k) {
+    const double x = ((valid >> k) & 1u) ? exp(s[k] - smax) : 0.0;
+    F[k] = (uint64_t)__double_as_longlong(x);
+    e += x;
+  }
   const double Z = wave_sum(e);
   const double zs = __ddiv_rn(kMassScale, Z);
   uint64_t tot = 0;
 #pragma unroll
   for (int k = 0; k < KPL; ++k) {
-    F[k] = ((valid >> k) & 1u) ? block_mass(s[k], smax, zs) : 0ull;
+    F[k] = ((valid >> k) & 1u) ? (uint64_t)__double2ull_rn(__dmul_rn(__longlong_as_double((long long)F[k]), zs)) : 0ull;
     tot += F[k];
   }
   const uint64_t total = wave_sum_u64(tot);
@@ -335,10 +342,10 @@ typedef double f64x4 __attribute__((ext_vector_type(4)));
 constexpr int kSelThreads = 512;  // 8 waves
 
 // Scores of 16 query blocks against every key block with the fp64 MFMA
-// (16x16x4): lane (row l%16, group g = l/16) feeds q_row[32g + ks] and
-// k_key[32g + ks] at step ks, so each lane reads 256 contiguous bytes per
-// operand and the 32 steps sum the full 128-dim dot product. Wave w takes key
-// tiles w, w+8, ...; then each wave selects rows w and w+8.
+// (16x16x4): lane (row l%16, group g = l/16) feeds the same head dim of its
+// query row and its key at each of 32 steps, the four groups covering
+// disjoint dims, so the 32 steps sum the full 128-dim dot product. Wave w
+// takes key tiles w, w+8, ...; then each wave selects rows w and w+8.
 template <int KPL>
 __global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __restrict__ qbar,
                                                                 const double* __restrict__ kbar, int nb, double p,
@@ -358,38 +365,56 @@ __global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __
   const int g = lane >> 4;
   const double inv_sqrt_d = 11.313708498984761;  // sqrt(128): s = dot / sqrt(128)
 
-  // A operand: q of row min(m16, rows-1), dims 32g .. 32g+31
+  // MFMA step k = 2u + e of lane (m16, g) multiplies dim 8u + 2g + e of
+  // query row m16 and key m16 of the tile: the four lane groups of one key
+  // read 64 contiguous bytes per load, two consecutive loads a whole line.
+  const int ntiles = (nb + 15) >> 4;
   double qa[32];
   {
-    const double* qr = qbar + ((int64_t)bh * nb + i0 + min(m16, rows - 1)) * kHeadDim + 32 * g;
+    const double* qr = qbar + ((int64_t)bh * nb + i0 + min(m16, rows - 1)) * kHeadDim + 2 * g;
 #pragma unroll
-    for (int k = 0; k < 32; k += 2) {
-      const double2 v = *reinterpret_cast<const double2*>(qr + k);
-      qa[k] = v.x;
-      qa[k + 1] = v.y;
+    for (int u = 0; u < 16; ++u) {
+      const double2 v = *reinterpret_cast<const double2*>(qr + 8 * u);
+      qa[2 * u] = v.x;
+      qa[2 * u + 1] = v.y;
     }
   }
-  const int ntiles = (nb + 15) >> 4;
-  const double* kb = kbar + (int64_t)bh * nb * kHeadDim;
-  for (int t = wave; t < ntiles; t += nwaves) {
-    const int key = t * 16 + m16;
-    const double* kr = kb + (int64_t)min(key, nb - 1) * kHeadDim + 32 * g;
-    double kk[32];
+  const double* kb = kbar + (int64_t)bh * nb * kHeadDim + 2 * g;
+  // Key tile t's operands load while tile t - 8 multiplies.
+  auto load_tile = [&](int t, double (&kk)[32]) {
+    const double* kr = kb + (int64_t)min(t * 16 + m16, nb - 1) * kHeadDim;
 #pragma unroll
-    for (int k = 0; k < 32; k += 2) {
-      const double2 v = *reinterpret_cast<const double2*>(kr + k);
-      kk[k] = v.x;
-      kk[k + 1] = v.y;
+    for (int u = 0; u < 16; ++u) {
+      const double2 v = *reinterpret_cast<const double2*>(kr + 8 * u);
+      kk[2 * u] = v.x;
+      kk[2 * u + 1] = v.y;
     }
+  };
+  auto score_tile = [&](int t, const double (&kk)[32]) {
     f64x4 acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
     for (int k = 0; k < 32; ++k) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[k], kk[k], acc, 0, 0, 0);
     // D layout of the fp64 16x16x4 MFMA: lane holds rows g + 4e (e = 0..3)
     // of key column m16.
+    const int key = t * 16 + m16;
     if (key < nb) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) sc[(g + 4 * e) * nb + key] = __ddiv_rn(acc[e], inv_sqrt_d);
     }
+  };
+  double ka[32], kn[32];
+  int t = wave;
+  if (t < ntiles) load_tile(t, ka);
+  while (t < ntiles) {
+    const int tn = t + nwaves;
+    if (tn < ntiles) load_tile(tn, kn);
+    score_tile(t, ka);
+    t = tn;
+    if (t >= ntiles) break;
+    const int tn2 = t + nwaves;
+    if (tn2 < ntiles) load_tile(tn2, ka);
+    score_tile(t, kn);
+    t = tn2;
   }
   __syncthreads();
 
