@@ -178,19 +178,13 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 a, f32x4 b) {
 
 __device__ __forceinline__ int ngroups_of(int n) { return (n + 31) >> 5; }
 
-// max / sum over lanes l, l^16, l^32, l^48 (the four lane groups holding one
+// max over lanes l, l^16, l^32, l^48 (the four lane groups holding one
 // query row) with the gfx950 lane-swap instructions; no LDS traffic.
 __device__ __forceinline__ float row_max4(float v) {
   const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
   const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-__device__ __forceinline__ float row_sum4(float v) {
-  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // Workgroup barrier without a memory fence: the only cross-wave traffic in
@@ -258,7 +252,13 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) o[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   float mrow[2] = {-1.0e30f, -1.0e30f};
-  float lrow[2] = {0.f, 0.f};
+  // Softmax denominators on the matrix unit: an extra O^T tile whose V^T
+  // operand is all ones accumulates sum_k P[k] for every query row (all 16
+  // rows of the tile hold it), rescaled together with O.
+  f32x4 lsum[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  bf16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
 
   // Lane constants of the transposing V reads: source lane 4e + q of group g4
   // points at row 32kg + 16hf + 4g4 + e, 8-byte chunk 4mt + q (swizzled).
@@ -388,7 +388,6 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
           negm[nt] = -mref * P.c2;
           mrow[nt] = mref;
         }
-        float rs[2] = {0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
           if (kk < ngh) {
@@ -399,9 +398,7 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
               for (int r = 0; r < 4; ++r) {
 #pragma unroll
                 for (int nt = 0; nt < 2; ++nt) {
-                  const float pv = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
-                  s[t][nt][r] = pv;
-                  rs[nt] += pv;
+                  s[t][nt][r] = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
                 }
               }
             }
@@ -411,10 +408,10 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         }
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
-          lrow[nt] = lrow[nt] * alpha[nt] + row_sum4(rs[nt]);
           if (__ballot(grow[nt])) {
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha[nt];
+            lsum[nt] *= alpha[nt];
           }
         }
       }
@@ -442,6 +439,8 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
               va = vn;
               __builtin_amdgcn_sched_barrier(0);
             }
+            lsum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][0], lsum[0], 0, 0, 0);
+            lsum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][1], lsum[1], 0, 0, 0);
           }
         }
       }
@@ -456,7 +455,7 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
       if (qtok[nt] >= 0) {
-        const float inv = lrow[nt] > 0.f ? 1.0f / lrow[nt] : 0.f;
+        const float inv = lsum[nt][0] > 0.f ? 1.0f / lsum[nt][0] : 0.f;
         uint16_t* orow = Oh + (uint32_t)(qtok[nt] * (int)P.sn + 4 * g4);
 #pragma unroll
         for (int mt = 0; mt < 8; ++mt) {
