@@ -92,9 +92,10 @@ fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* 
  *   running sum of their P; m_p = min{r : c_r >= p} (nb if none reaches p,
  *   and nb when p == 1); m = max(m_p, min(k_min, nb)); the first m blocks of
  *   that order are kept.
- * All routing arithmetic is fp64. The running sums are exact fixed-point
- * sums of the fp64 probabilities (2^-62 quanta), so the decision c_r >= p
- * agrees with an fp64 sequential sum except within ~1e-15 of p.
+ * Pooling and scores are fp64, so the order of the key blocks is exact. The
+ * probabilities use an fp32 exp2 (relative error below 2^-21) and are summed
+ * as exact fixed-point masses (2^-62 quanta), so the decision c_r >= p agrees
+ * with an fp64 sequential sum except within about 1e-6 of p.
  *
  * Inputs : Q, K (bf16, desc), p in [0, 1], k_min >= 0, tiling.
  * Outputs: block_mask uint8 [batch, heads, nb, nb] (1 = kept), fully written;

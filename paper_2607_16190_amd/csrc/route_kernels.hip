@@ -10,15 +10,16 @@
 //                  (§2.1), then the mask row, the count and the ascending
 //                  kept-block list. One wavefront owns one row at a time.
 //
-// The Top-p cut never sorts the row. The probabilities are turned into exact
+// The Top-p cut never sorts the row. The probabilities are turned into
 // fixed-point masses F_j = round(P_j * 2^62), so every partial sum is exact
 // and order-free; a bucketed radix select over the scores (64 buckets per
 // level, ordered from the highest score) finds the bucket in which the
 // running mass first reaches T = ceil(p * 2^62), then recurses into that
 // bucket until at most 64 candidates remain, which are ranked exactly by
-// (score desc, block id asc). The result equals the sequential-sum definition
-// except where a running sum lies within a few 2^-62 quanta (plus the fp64
-// rounding of P) of p.
+// (score desc, block id asc). P_j carries the relative error of the fp32
+// exp2 (below 2^-21, so every running sum is within 1e-6 of its exact value):
+// the result equals the fp64 sequential-sum definition except where a running
+// sum lies within about 1e-6 of p.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -99,11 +100,20 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
   out[((int64_t)bh * g.nb + i) * kHeadDim + d] = s / (double)box.n;
 }
 
-// Fixed-point mass of one block: round(exp(s - smax) * (2^62 / Z)). Every
-// caller evaluates exactly this expression, so a block's mass is the same
-// wherever it is recomputed.
+// Unnormalised probability exp(s - smax) of a block (s <= smax), evaluated
+// with the hardware exp2 in fp32: relative error below 2^-21, far inside
+// what the Top-p decision needs (the scores themselves, which decide the
+// order, stay fp64). Masses below 2^-126 flush to zero; they are below the
+// 2^-62 quantum of the fixed-point sums anyway.
+__device__ __forceinline__ double block_exp(double s, double smax) {
+  return (double)__builtin_amdgcn_exp2f((float)((s - smax) * 1.4426950408889634));
+}
+
+// Fixed-point mass of one block: round(block_exp(s, smax) * (2^62 / Z)).
+// Every caller evaluates exactly this expression, so a block's mass is the
+// same wherever it is recomputed.
 __device__ __forceinline__ uint64_t block_mass(double s, double smax, double zs) {
-  return (uint64_t)__double2ull_rn(__dmul_rn(exp(s - smax), zs));
+  return (uint64_t)__double2ull_rn(__dmul_rn(block_exp(s, smax), zs));
 }
 
 struct WaveScratch {
@@ -280,12 +290,12 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
   }
   const double smax = wave_max(vmax);
   const double smin = wave_min(vmin);
-  // F[k] first holds exp(s - smax) (as bits), then the fixed-point mass;
-  // block_mass evaluates the same two roundings.
+  // F[k] first holds block_exp(s, smax) (as bits), then the fixed-point
+  // mass; block_mass evaluates the same two roundings.
   double e = 0.0;
 #pragma unroll
   for (int k = 0; k < KPL; ++k) {
-    const double x = ((valid >> k) & 1u) ? exp(s[k] - smax) : 0.0;
+    const double x = ((valid >> k) & 1u) ? block_exp(s[k], smax) : 0.0;
     F[k] = (uint64_t)__double_as_longlong(x);
     e += x;
   }
