@@ -176,7 +176,10 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 a, f32x4 b) {
   return __builtin_convertvector(v, bf16x8);
 }
 
-__device__ __forceinline__ int ngroups_of(int n) { return (n + 31) >> 5; }
+// Key groups (of 32) a block is processed with: blocks of at most 64 keys
+// take one 64-key half, all others both halves (keys past n are masked).
+// With only these two shapes every half runs with constant loop bounds.
+__device__ __forceinline__ int ngroups_of(int n) { return n <= 64 ? 2 : 4; }
 
 // max over lanes l, l^16, l^32, l^48 (the four lane groups holding one
 // query row) with the gfx950 lane-swap instructions; no LDS traffic.
@@ -301,18 +304,18 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
     // most 64 real keys is empty.
 #pragma unroll
     for (int hb = 0; hb < 2; ++hb) {
-      const int ngh = min(max(ng - 2 * hb, 0), 2);  // key groups in this half
+      const int ngh = ng > 2 * hb ? 2 : 0;  // key groups in this half (0 or 2)
       f32x4 s[4][2];
       if (active && ngh > 0) {
-        // S^T = K Q^T for LDS tiles 4hb .. 4hb + 2ngh - 1; the fragments of
-        // tile t+1 load while tile t multiplies.
+        // S^T = K Q^T for LDS tiles 4hb .. 4hb + 3; the fragments of tile t+1
+        // load while tile t multiplies.
         bf16x8 ka[4], kn[4];
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) ka[ks] = kfrag(4 * hb, ks);
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          if (t < 2 * ngh) {
-            if (t + 1 < 2 * ngh) {
+          if (t < 4) {
+            if (t + 1 < 4) {
 #pragma unroll
               for (int ks = 0; ks < 4; ++ks) kn[ks] = kfrag(4 * hb + t + 1, ks);
             }
@@ -347,10 +350,10 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
       if (active && ngh > 0) {
         // Online softmax over this half. Accumulator (t, r) of lane group g4
         // holds key 64hb + 32*(t/2) + 8*g4 + 4*(t%2) + r.
-        if (nj < 64 * hb + 32 * ngh) {
+        if (nj < 64 * hb + 64) {
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            if (t < 2 * ngh) {
+            if (t < 4) {
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
                 const int kap = 64 * hb + 32 * (t >> 1) + 8 * g4 + 4 * (t & 1) + r;
@@ -365,7 +368,7 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         float mx[2] = {-INFINITY, -INFINITY};
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          if (t < 2 * ngh) {
+          if (t < 4) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               mx[0] = fmaxf(mx[0], s[t][0][r]);
@@ -390,7 +393,7 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         }
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-          if (kk < ngh) {
+          if (kk < 2) {
 #pragma unroll
             for (int hh = 0; hh < 2; ++hh) {
               const int t = 2 * kk + hh;
@@ -428,12 +431,12 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         bf16x8 va = vfrag(2 * hb, 0);
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-          if (kk < ngh) {
+          if (kk < 2) {
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) {
               bf16x8 vn = va;
               if (mt + 1 < 8) vn = vfrag(2 * hb + kk, mt + 1);
-              else if (kk + 1 < ngh) vn = vfrag(2 * hb + kk + 1, 0);
+              else if (kk + 1 < 2) vn = vfrag(2 * hb + kk + 1, 0);
               o[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][0], o[mt][0], 0, 0, 0);
               o[mt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][1], o[mt][1], 0, 0, 0);
               va = vn;
