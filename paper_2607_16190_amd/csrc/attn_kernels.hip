@@ -307,29 +307,22 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
       const int ngh = ng > 2 * hb ? 2 : 0;  // key groups in this half (0 or 2)
       f32x4 s[4][2];
       if (active && ngh > 0) {
-        // S^T = K Q^T for LDS tiles 4hb .. 4hb + 3; the fragments of tile t+1
-        // load while tile t multiplies.
-        bf16x8 ka[4], kn[4];
+        // S^T = K Q^T for LDS tiles 4hb .. 4hb + 3. Step u = 4t + ks; the K
+        // fragment of step u + 3 is read while step u multiplies (a ring of
+        // four fragments), so the LDS latency is covered by six MFMAs.
+        constexpr int kKPre = 3;
+        bf16x8 kq[kKPre + 1];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) ka[ks] = kfrag(4 * hb, ks);
+        for (int u = 0; u < kKPre; ++u) kq[u] = kfrag(4 * hb + (u >> 2), u & 3);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          if (t < 4) {
-            if (t + 1 < 4) {
-#pragma unroll
-              for (int ks = 0; ks < 4; ++ks) kn[ks] = kfrag(4 * hb + t + 1, ks);
-            }
-            s[t][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-            s[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-              s[t][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qf[0][ks], s[t][0], 0, 0, 0);
-              s[t][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qf[1][ks], s[t][1], 0, 0, 0);
-            }
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) ka[ks] = kn[ks];
-            __builtin_amdgcn_sched_barrier(0);
-          }
+        for (int u = 0; u < 16; ++u) {
+          const int t = u >> 2, ks = u & 3;
+          if (u + kKPre < 16) kq[(u + kKPre) % (kKPre + 1)] = kfrag(4 * hb + ((u + kKPre) >> 2), (u + kKPre) & 3);
+          const bf16x8 ka = kq[u % (kKPre + 1)];
+          const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+          s[t][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[0][ks], ks == 0 ? z : s[t][0], 0, 0, 0);
+          s[t][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[1][ks], ks == 0 ? z : s[t][1], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
       if (hb == 1) {
@@ -427,24 +420,25 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
 
       if (active && ngh > 0) {
         // O^T += V^T P^T, 32 keys per MFMA; V^T comes from row-major V through
-        // transposing LDS reads; step t+1's fragment loads while step t runs.
-        bf16x8 va = vfrag(2 * hb, 0);
+        // transposing LDS reads. Step u = 8kk + mt; the fragment of step u + 3
+        // is read while step u multiplies (a ring of four fragments), so the
+        // LDS latency is covered by six MFMAs.
+        constexpr int kVPre = 3;
+        bf16x8 vq[kVPre + 1];
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          if (kk < 2) {
+        for (int u = 0; u < kVPre; ++u) vq[u] = vfrag(2 * hb + (u >> 3), u & 7);
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) {
-              bf16x8 vn = va;
-              if (mt + 1 < 8) vn = vfrag(2 * hb + kk, mt + 1);
-              else if (kk + 1 < 2) vn = vfrag(2 * hb + kk + 1, 0);
-              o[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][0], o[mt][0], 0, 0, 0);
-              o[mt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][1], o[mt][1], 0, 0, 0);
-              va = vn;
-              __builtin_amdgcn_sched_barrier(0);
-            }
+        for (int u = 0; u < 16; ++u) {
+          const int kk = u >> 3, mt = u & 7;
+          if (u + kVPre < 16) vq[(u + kVPre) % (kVPre + 1)] = vfrag(2 * hb + ((u + kVPre) >> 3), (u + kVPre) & 7);
+          const bf16x8 va = vq[u % (kVPre + 1)];
+          o[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][0], o[mt][0], 0, 0, 0);
+          o[mt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][1], o[mt][1], 0, 0, 0);
+          if (mt == 7) {
             lsum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][0], lsum[0], 0, 0, 0);
             lsum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][1], lsum[1], 0, 0, 0);
           }
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
