@@ -122,9 +122,11 @@ __device__ __forceinline__ void row_offsets(const AttnParams& P, const BlockMap&
   const int sn2 = 2 * (int)P.sn;  // bytes per token row
   const int W = P.g.W;
   const int HW = P.g.H * P.g.W;
-  if (m.plane == 64 && m.ex == 8) {
-    // Full 8x8 planes: kap / 64 = w / 2, (kap / 8) % 8 = 4(w % 2) + u % 4,
-    // kap % 8 = 4(u / 4) + lq, and every row is real (n = 64 or 128).
+  if (m.n == 128 && m.plane == 64 && m.ex == 8) {
+    // Two full 8x8 planes: kap / 64 = w / 2, (kap / 8) % 8 = 4(w % 2) + u % 4,
+    // kap % 8 = 4(u / 4) + lq, and every row is real. Other blocks (a single
+    // plane included) take the general path, whose rows past n repeat the
+    // last real row.
     const int a = (m.tbase + (w >> 1) * HW + 4 * (w & 1) * W) * sn2;  // wave-uniform
     const int l = lq * sn2;
 #pragma unroll
@@ -539,9 +541,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
 // in the shared last-level cache) and the resident workgroups of one XCD
 // work on neighbouring query blocks (their kept K/V blocks overlap in L2).
 // Scratch per head: cost, rank, run starts [kQueues + 1], queue offsets [kQueues].
-__global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ counts, int n_heads, int nb,
+__global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ counts, int n_heads, Geometry g,
                                                    int32_t* __restrict__ items, int32_t* __restrict__ qbase,
                                                    int32_t* __restrict__ qctr, int32_t* __restrict__ hscratch) {
+  const int nb = g.nb;
   int32_t* hcost = hscratch;
   int32_t* horder = hcost + n_heads;
   int32_t* hstart = horder + n_heads;                  // [n_heads][kQueues + 1]
@@ -549,8 +552,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
-  auto cost_of = [&](int h, int i) {
-    const int c = counts[(int64_t)h * nb + i];
+  auto cost_of = [&](int h, int r) {
+    const int c = counts[(int64_t)h * nb + r];
     return (c < 0 ? 0 : (c > nb ? nb : c)) + 1;
   };
 
@@ -764,7 +767,7 @@ hipError_t launch_attn(const AttnArgs& a) {
     hipLaunchKernelGGL(attn_naive_kernel, dim3(n_items), dim3(kAttnThreads), 0, a.stream, P);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, a.batch * a.heads, g.nb, ws.items,
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, a.batch * a.heads, g, ws.items,
                      ws.qbase, ws.qctr, ws.hscratch);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
