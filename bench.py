@@ -143,7 +143,9 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0):
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each scaled by the factor the same
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
-ATTN_TRAFFIC = {"source_digest": "14e1ab749cf0a865", "workload": "720p", "bytes": 211091655680 + 775206000}
+ATTN_TRAFFIC = {"source_digest": "dc73de173e08185e", "workload": "720p", "bytes": 235912492093 + 775236160}
+# Same for fva_route (pool_kernel + select_kernel), per call on the 720p workload.
+ROUTE_TRAFFIC = {"source_digest": "b4d21ba48bd95b23", "workload": "720p", "bytes": (756006 + 126133) * 2048 + (52800 + 49132) * 1024}
 
 
 def copy_calibration(torch, gib=1.0, reps=5):
@@ -262,6 +264,10 @@ def main():
     traffic = None
     if ATTN_TRAFFIC["source_digest"] == digest and ATTN_TRAFFIC["workload"] == cfg.name and args.sched == "persistent":
         traffic = ATTN_TRAFFIC["bytes"]
+    route_digest = source_digest(os.path.join(here, "paper_2607_16190_amd", "csrc", "route_kernels.hip"))
+    route_traffic = None
+    if ROUTE_TRAFFIC["source_digest"] == route_digest and ROUTE_TRAFFIC["workload"] == cfg.name:
+        route_traffic = ROUTE_TRAFFIC["bytes"]
     res = {
         "metric": METRIC,
         "value": round(dense_flops / (ms_per_step / 1e3) / 1e12, 2),
@@ -290,6 +296,15 @@ def main():
         "route_us": round(t_route * 1e6, 2),
         "route_GBps": round(route_bytes / t_route / 1e9, 1),
         "route_frac_hbm": round(route_bytes / t_route / 1e9 / PEAK_HBM_GBPS, 4),
+        "route_roofline": {
+            "bound": "hbm",
+            "achieved": round(route_bytes / t_route / 1e9, 1),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(route_bytes / t_route / 1e9 / PEAK_HBM_GBPS, 4),
+            "traffic": route_traffic,
+            "algorithmic_bytes_per_call": route_bytes,
+        },
         "kept_tile_TFLOPS": round(kept_tile_flops / t_attn / 1e12, 2),
         "kept_tile_frac_bf16_peak": round(kept_tile_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS, 4),
         "useful_TFLOPS": round(useful_flops / t_attn / 1e12, 2),
