@@ -188,3 +188,36 @@ def test_attn_deterministic_and_trace():
     tr = trace.view(-1, 4).cpu().numpy()
     assert tr.shape[0] == cfg.heads * geo.nb
     assert np.all(tr[:, 1] >= tr[:, 0]) and np.all(tr[:, 0] > 0)
+
+
+def test_attn_max_blocks_sampled():
+    # nb = 1024, the largest supported block count; sampled query blocks.
+    fva = lib()
+    cfg = custom_config("max_blocks", 1, (16, 128, 64), (2, 8, 8), (1.5,), seed=11)
+    geo = geometry_of(cfg)
+    assert geo.nb == 1024
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    q, k, v = upload(Qb, Kb, Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    O = run_attn(q, k, v, cfg, mask, counts, kv)
+    m = mask.cpu().numpy()[0, 0]
+    rows = [0, 7, 511, 512, 1000, 1023]
+    ref = attn_ref_rows(f64(Qb[0, 0]), f64(Kb[0, 0]), f64(Vb[0, 0]), m, geo, rows)
+    Of = O[0, 0].float().cpu().numpy()
+    e = np.concatenate([np.abs(Of[geo.block_tokens[i]] - o).ravel() for i, o in ref.items()])
+    log(f"[attn] max_blocks: rows {rows}, max abs {e.max():.3e} mean abs {e.mean():.3e}")
+    assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
+
+
+def test_attn_batch_two_odd_heads():
+    fva = lib()
+    cfg = synth.WorkloadConfig("batch2", 3, (5, 13, 21), (2, 8, 8), 0.9, 3, 12, "fixed", (0.7, 2.5, 4.0), batch=2)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    q, k, v = upload(Qb, Kb, Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    O_p = run_attn(q, k, v, cfg, mask, counts, kv)
+    O_n = run_attn(q, k, v, cfg, mask, counts, kv, flags=fva.FVA_SCHED_NAIVE)
+    O_m = run_attn(q, k, v, cfg, mask)
+    torch = torch_mod()
+    assert torch.equal(O_p, O_n) and torch.equal(O_p, O_m)
+    compare_full("batch2", Qb, Kb, Vb, cfg, mask.cpu().numpy(), o64(O_p))

@@ -127,3 +127,18 @@ def test_route_deterministic():
     assert np.array_equal(m1, m2) and np.array_equal(c1, c2)
     valid = np.arange(k1.shape[-1])[None, None, None, :] < c1[..., None]
     assert np.array_equal(k1[valid], k2[valid])  # entries past counts are unspecified
+
+
+def test_route_max_blocks():
+    # nb = 1024, the largest supported block count: 16 x 128 x 64 tokens, 2x8x8 boxes.
+    cfg = custom_config("max_blocks", 1, (16, 128, 64), (2, 8, 8), (1.5,), seed=11)
+    assert geometry_of(cfg).nb == 1024
+    Qb, Kb, _ = synth.gen_qkv(cfg)
+    check_route("max_blocks", Qb, Kb, cfg, cfg.p, cfg.k_min)
+
+
+def test_route_batch_two_odd_heads():
+    cfg = synth.WorkloadConfig("batch2", 3, (5, 13, 21), (2, 8, 8), 0.9, 3, 12, "fixed", (0.7, 2.5, 4.0), batch=2)
+    Qb, Kb, _ = synth.gen_qkv(cfg)
+    assert Qb.shape[:2] == (2, 3)
+    check_route("batch2", Qb, Kb, cfg, cfg.p, cfg.k_min)
