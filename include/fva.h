@@ -78,7 +78,8 @@ int32_t fva_num_blocks(const fva_tiling* tiling);
 
 /*
  * Workspace bytes needed by fva_route for this shape: the pooled block means
- * of Q and K in fp64, 2 * batch*heads*nb*128*8 bytes, 256-byte aligned.
+ * of Q and K in fp64 with nb rounded up to a multiple of 16,
+ * 2 * batch*heads*ceil16(nb)*128*8 bytes, 256-byte aligned.
  */
 fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes);
 

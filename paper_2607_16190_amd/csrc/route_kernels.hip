@@ -2,9 +2,9 @@
 //
 // pool_kernel   -- qbar_i, kbar_i = fp64 means of Q, K over the real tokens
 //                  of block i (pooled block similarities, §3.1). One workgroup
-//                  per (b, h, i) streams the block's rows of Q and K once;
-//                  sixteen lanes cover one 256-byte token row, so every wave
-//                  load is a run of whole rows.
+//                  per (b, h) and 8 consecutive blocks streams their rows of
+//                  Q and K once (sixteen lanes per 256-byte token row) and
+//                  writes the means as whole lines in MFMA operand order.
 // select_kernel -- for 16 query blocks of one (b, h): fp64 scores against
 //                  every key block, softmax, Top-p cut with the Top-k floor
 //                  (§2.1), then the mask row, the count and the ascending
@@ -31,73 +31,126 @@ namespace fva {
 
 namespace {
 
-constexpr int kPoolThreads = 256;
+constexpr int kPoolThreads = 512;  // one wavefront per block, 8 blocks
 constexpr int kSelRows = 16;         // query blocks per select workgroup
 constexpr double kMassScale = 4611686018427387904.0;  // 2^62
 
+// Pooled means are stored in the operand order of the fp64 16x16x4 MFMA of
+// select_kernel: per head, tiles of 16 blocks; within tile T, load step u
+// (0..15) holds 64 lanes x 2 doubles, lane 16g + m carrying dims 32g + 2u and
+// 32g + 2u + 1 of block 16T + m. Every operand load of a tile is one
+// contiguous kilobyte, and the 8 blocks of a pool workgroup fill whole
+// 128-byte lines. Blocks are padded to a multiple of 16 (the padding means
+// are zero and never read as real blocks).
+__host__ __device__ constexpr int padded_blocks(int nb) { return (nb + 15) & ~15; }
+constexpr int kPoolBlocks = 8;  // blocks per pool workgroup (half an operand tile)
+
+// One workgroup pools blocks 8G .. 8G + 7 of one (b, h), one wavefront per
+// block: lane (slot = lane / 16, chunk c = lane % 16) sums dims 8c .. 8c+7 of
+// Q and K over rows slot, slot + 4, ... in fp64 (each wave load is four whole
+// 256-byte token rows), the four slots are summed across lanes, and the
+// means are staged in operand order; the group's 16 KB of Q and K means are
+// then written as whole lines.
+constexpr int kPoolRowsPerStep = 16;  // token rows each lane loads per step
+static_assert(kPoolThreads == 64 * kPoolBlocks, "one wavefront per pooled block");
 __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __restrict__ Q,
                                                            const uint16_t* __restrict__ K, int heads,
                                                            int64_t sb, int64_t sh, int64_t sn, Geometry g,
                                                            double* __restrict__ qbar,
                                                            double* __restrict__ kbar) {
-  __shared__ double red[2][16][kHeadDim];
-  const int i = blockIdx.x;
+  __shared__ double stage[2][16 * 4 * kPoolBlocks * 2];  // [tensor][u][g][block][pair]
+  const int wave = threadIdx.x >> 6;  // block i0 + wave
+  const int lane = threadIdx.x & 63;
+  const int i0 = blockIdx.x * kPoolBlocks;
+  const int i = i0 + wave;
   const int bh = blockIdx.y;
-  const int b = bh / heads;
-  const int h = bh - b * heads;
-  const int64_t base = (int64_t)b * sb + (int64_t)h * sh;
-  const BlockBox box = block_box(g, i);
-  const int c = threadIdx.x & 15;    // 16-byte chunk: dims 8c .. 8c+7
-  const int slot = threadIdx.x >> 4;  // token slot 0..15
-
-  // Row r = slot + 16u of the block. For full 8x8 planes, r / 64, (r / 8) % 8
-  // and r % 8 are (u / 4, 2(u % 4) + slot / 8, slot % 8): no divisions.
-  const bool fast = box.ey == 8 && box.ex == 8;
-  const int HW = g.H * g.W;
-  const int tb = (box.t0 * g.H + box.y0) * g.W + box.x0;
-  const int lane_tok = (slot >> 3) * g.W + (slot & 7);
-  uint4 vq[8], vk[8];
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int r = slot + 16 * u;
-    if (r < box.n) {
-      const int tok = fast ? tb + (u >> 2) * HW + 2 * (u & 3) * g.W + lane_tok : box_token(g, box, r);
-      const int64_t off = base + (int64_t)tok * sn + c * 8;
-      vq[u] = *reinterpret_cast<const uint4*>(Q + off);
-      vk[u] = *reinterpret_cast<const uint4*>(K + off);
-    } else {
-      vq[u] = make_uint4(0, 0, 0, 0);
-      vk[u] = make_uint4(0, 0, 0, 0);
-    }
-  }
+  const int c = lane & 15;     // 16-byte chunk: dims 8c .. 8c+7
+  const int slot = lane >> 4;  // rows slot + 4j
   double aq[8], ak[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) { aq[e] = 0.0; ak[e] = 0.0; }
+  double nreal = 1.0;
+  if (i < g.nb) {
+    const int b = bh / heads;
+    const int h = bh - b * heads;
+    const int64_t base = (int64_t)b * sb + (int64_t)h * sh + c * 8;
+    const BlockBox box = block_box(g, i);
+    nreal = (double)box.n;
+    const int jend = (box.n + 4 * kPoolRowsPerStep - 1) / (4 * kPoolRowsPerStep) * kPoolRowsPerStep;
+    // For full 8x8 planes, row r = slot + 4j sits at plane j / 16, line
+    // (j / 2) % 8, column slot + 4 (j % 2): no divisions.
+    const bool fast = box.ey == 8 && box.ex == 8;
+    const int HW = g.H * g.W;
+    const int tb = (box.t0 * g.H + box.y0) * g.W + box.x0 + slot;
+    for (int j0 = 0; j0 < jend; j0 += kPoolRowsPerStep) {
+      uint4 vq[kPoolRowsPerStep], vk[kPoolRowsPerStep];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const uint32_t wq[4] = {vq[u].x, vq[u].y, vq[u].z, vq[u].w};
-    const uint32_t wk[4] = {vk[u].x, vk[u].y, vk[u].z, vk[u].w};
+      for (int jj = 0; jj < kPoolRowsPerStep; ++jj) {
+        const int j = j0 + jj;
+        const int r = slot + 4 * j;
+        if (r < box.n) {
+          const int tok = fast ? tb + (j >> 4) * HW + ((j >> 1) & 7) * g.W + 4 * (j & 1) : box_token(g, box, r);
+          const int64_t off = base + (int64_t)tok * sn;
+          vq[jj] = *reinterpret_cast<const uint4*>(Q + off);
+          vk[jj] = *reinterpret_cast<const uint4*>(K + off);
+        } else {
+          vq[jj] = make_uint4(0, 0, 0, 0);
+          vk[jj] = make_uint4(0, 0, 0, 0);
+        }
+      }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      aq[2 * e] += (double)bf16_lo(wq[e]);
-      aq[2 * e + 1] += (double)bf16_hi(wq[e]);
-      ak[2 * e] += (double)bf16_lo(wk[e]);
-      ak[2 * e + 1] += (double)bf16_hi(wk[e]);
+      for (int jj = 0; jj < kPoolRowsPerStep; ++jj) {
+        const uint32_t wq[4] = {vq[jj].x, vq[jj].y, vq[jj].z, vq[jj].w};
+        const uint32_t wk[4] = {vk[jj].x, vk[jj].y, vk[jj].z, vk[jj].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          aq[2 * e] += (double)bf16_lo(wq[e]);
+          aq[2 * e + 1] += (double)bf16_hi(wq[e]);
+          ak[2 * e] += (double)bf16_lo(wk[e]);
+          ak[2 * e + 1] += (double)bf16_hi(wk[e]);
+        }
+      }
     }
   }
+  // Sum the four slots: lanes c, c + 16, c + 32, c + 48.
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    red[0][slot][c * 8 + e] = aq[e];
-    red[1][slot][c * 8 + e] = ak[e];
+    aq[e] += __shfl_xor(aq[e], 16);
+    ak[e] += __shfl_xor(ak[e], 16);
+    aq[e] += __shfl_xor(aq[e], 32);
+    ak[e] += __shfl_xor(ak[e], 32);
+  }
+  // Slot 0 stores the Q means, slot 1 the K means (zero for padding blocks):
+  // dims 8c + 2v, 8c + 2v + 1 are pair (u, g) = (4 (c % 4) + v, c / 4).
+  if (slot < 2) {
+    double* st = stage[slot];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const double x0 = slot ? ak[2 * v] : aq[2 * v];
+      const double x1 = slot ? ak[2 * v + 1] : aq[2 * v + 1];
+      const int u = 4 * (c & 3) + v;
+      double2 m2;
+      m2.x = i < g.nb ? x0 / nreal : 0.0;
+      m2.y = i < g.nb ? x1 / nreal : 0.0;
+      *reinterpret_cast<double2*>(&st[((u * 4 + (c >> 2)) * kPoolBlocks + wave) * 2]) = m2;
+    }
   }
   __syncthreads();
-  const int which = threadIdx.x >> 7;  // 0: Q, 1: K
-  const int d = threadIdx.x & 127;
-  double s = 0.0;
+  // 2 x 512 chunks of 16 bytes: chunk q of a tensor is (u, g, m) = (q / 32,
+  // (q / 8) % 4, q % 8); eight consecutive threads write one 128-byte line.
+  const int tile = i0 >> 4;
+  const int hm = (i0 >> 3) & 1;  // which 8 blocks of the 16-block tile
+  const int64_t head_off = (int64_t)bh * padded_blocks(g.nb) * kHeadDim;
 #pragma unroll
-  for (int k = 0; k < 16; ++k) s += red[which][k][d];
-  double* out = which ? kbar : qbar;
-  out[((int64_t)bh * g.nb + i) * kHeadDim + d] = s / (double)box.n;
+  for (int k = 0; k < 2; ++k) {
+    const int q = threadIdx.x + kPoolThreads * k;  // 0 .. 1023 over both tensors
+    const int t = q >> 9;
+    const int qq = q & 511;
+    const int u = qq >> 5, gg = (qq >> 3) & 3, m = qq & 7;
+    const double2 v = *reinterpret_cast<const double2*>(&stage[t][((u * 4 + gg) * kPoolBlocks + m) * 2]);
+    double* out = (t ? kbar : qbar) + head_off + ((int64_t)(tile * 16 + u) * 64 + gg * 16 + hm * 8 + m) * 2;
+    *reinterpret_cast<double2*>(out) = v;
+  }
 }
 
 // Unnormalised probability exp(s - smax) of a block (s <= smax), evaluated
@@ -352,10 +405,10 @@ typedef double f64x4 __attribute__((ext_vector_type(4)));
 constexpr int kSelThreads = 512;  // 8 waves
 
 // Scores of 16 query blocks against every key block with the fp64 MFMA
-// (16x16x4): lane (row l%16, group g = l/16) feeds the same head dim of its
-// query row and its key at each of 32 steps, the four groups covering
-// disjoint dims, so the 32 steps sum the full 128-dim dot product. Wave w
-// takes key tiles w, w+8, ...; then each wave selects rows w and w+8.
+// (16x16x4): lane (row l%16, group g = l/16) feeds dim 32g + k of its query
+// row and its key at step k, so the 32 steps sum the full 128-dim dot
+// product. Wave w takes key tiles w, w+8, ...; then each wave selects rows w
+// and w+8.
 template <int KPL>
 __global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __restrict__ qbar,
                                                                 const double* __restrict__ kbar, int nb, double p,
@@ -375,27 +428,29 @@ __global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __
   const int g = lane >> 4;
   const double inv_sqrt_d = 11.313708498984761;  // sqrt(128): s = dot / sqrt(128)
 
-  // MFMA step k = 2u + e of lane (m16, g) multiplies dim 8u + 2g + e of
-  // query row m16 and key m16 of the tile: the four lane groups of one key
-  // read 64 contiguous bytes per load, two consecutive loads a whole line.
+  // Operands in the order written by pool_kernel: MFMA step k = 2u + e of
+  // lane (m16, g) multiplies dim 32g + 2u + e of query row m16 and key m16 of
+  // the tile; each load is one contiguous kilobyte. Rows and keys of the last
+  // tile past nb are padding (zero means): their scores are never stored.
   const int ntiles = (nb + 15) >> 4;
+  const int64_t head_off = (int64_t)bh * padded_blocks(nb) * kHeadDim;
   double qa[32];
   {
-    const double* qr = qbar + ((int64_t)bh * nb + i0 + min(m16, rows - 1)) * kHeadDim + 2 * g;
+    const double* qr = qbar + head_off + (int64_t)blockIdx.x * 16 * kHeadDim + 2 * lane;
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
-      const double2 v = *reinterpret_cast<const double2*>(qr + 8 * u);
+      const double2 v = *reinterpret_cast<const double2*>(qr + u * 128);
       qa[2 * u] = v.x;
       qa[2 * u + 1] = v.y;
     }
   }
-  const double* kb = kbar + (int64_t)bh * nb * kHeadDim + 2 * g;
+  const double* kb = kbar + head_off + 2 * lane;
   // Key tile t's operands load while tile t - 8 multiplies.
   auto load_tile = [&](int t, double (&kk)[32]) {
-    const double* kr = kb + (int64_t)min(t * 16 + m16, nb - 1) * kHeadDim;
+    const double* kr = kb + (int64_t)t * 16 * kHeadDim;
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
-      const double2 v = *reinterpret_cast<const double2*>(kr + 8 * u);
+      const double2 v = *reinterpret_cast<const double2*>(kr + u * 128);
       kk[2 * u] = v.x;
       kk[2 * u + 1] = v.y;
     }
@@ -455,7 +510,7 @@ hipError_t launch_select(const RouteArgs& a, int nb, double* qbar, double* kbar)
 }  // namespace
 
 size_t route_workspace_bytes(int batch, int heads, int nb) {
-  const size_t one = (size_t)batch * heads * nb * kHeadDim * sizeof(double);
+  const size_t one = (size_t)batch * heads * padded_blocks(nb) * kHeadDim * sizeof(double);
   const size_t aligned = (one + 255) & ~(size_t)255;
   return 2 * aligned;
 }
@@ -465,10 +520,10 @@ hipError_t launch_route(const RouteArgs& a) {
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
   const int bhs = a.batch * a.heads;
   if (bhs == 0) return hipSuccess;
-  const size_t one = ((size_t)bhs * g.nb * kHeadDim * sizeof(double) + 255) & ~(size_t)255;
+  const size_t one = ((size_t)bhs * padded_blocks(g.nb) * kHeadDim * sizeof(double) + 255) & ~(size_t)255;
   double* qbar = reinterpret_cast<double*>(a.workspace);
   double* kbar = reinterpret_cast<double*>(reinterpret_cast<char*>(a.workspace) + one);
-  hipLaunchKernelGGL(pool_kernel, dim3(g.nb, bhs), dim3(kPoolThreads), 0, a.stream,
+  hipLaunchKernelGGL(pool_kernel, dim3(padded_blocks(g.nb) / kPoolBlocks, bhs), dim3(kPoolThreads), 0, a.stream,
                      reinterpret_cast<const uint16_t*>(a.Q), reinterpret_cast<const uint16_t*>(a.K), a.heads,
                      a.stride_b, a.stride_h, a.stride_n, g, qbar, kbar);
   hipError_t e = hipGetLastError();
