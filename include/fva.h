@@ -78,8 +78,9 @@ int32_t fva_num_blocks(const fva_tiling* tiling);
 
 /*
  * Workspace bytes needed by fva_route for this shape: the pooled block means
- * of Q and K in fp64 with nb rounded up to a multiple of 16,
- * 2 * batch*heads*ceil16(nb)*128*8 bytes, 256-byte aligned.
+ * of Q and K in fp64 with nb rounded up to a multiple of 16
+ * (2 * batch*heads*ceil16(nb)*128*8 bytes) and the fp64 block scores
+ * (batch*heads*nb*nb*8 bytes), each part 256-byte aligned.
  */
 fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes);
 
@@ -95,7 +96,7 @@ fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* 
  *   that order are kept.
  * Pooling and scores are fp64, so the order of the key blocks is exact. The
  * probabilities use an fp32 exp2 (relative error below 2^-21) and are summed
- * as exact fixed-point masses (2^-62 quanta), so the decision c_r >= p agrees
+ * as exact fixed-point masses (2^-52 quanta), so the decision c_r >= p agrees
  * with an fp64 sequential sum except within about 1e-6 of p.
  *
  * Inputs : Q, K (bf16, desc), p in [0, 1], k_min >= 0, tiling.

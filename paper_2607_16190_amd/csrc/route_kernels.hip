@@ -11,12 +11,12 @@
 //                  kept-block list. One wavefront owns one row at a time.
 //
 // The Top-p cut never sorts the row. The probabilities are turned into
-// fixed-point masses F_j = round(P_j * 2^62), so every partial sum is exact
+// fixed-point masses F_j = round(P_j * 2^52), so every partial sum is exact
 // and order-free; a bucketed radix select over the scores (64 buckets per
 // level, ordered from the highest score) finds the bucket in which the
-// running mass first reaches T = ceil(p * 2^62), then recurses into that
-// bucket until at most 64 candidates remain, which are ranked exactly by
-// (score desc, block id asc). P_j carries the relative error of the fp32
+// running mass first reaches T = ceil(p * 2^52), then recurses into that
+// bucket until at most 64 candidates remain, whose order is then resolved
+// exactly by (score desc, block id asc). P_j carries the relative error of the fp32
 // exp2 (below 2^-21, so every running sum is within 1e-6 of its exact value):
 // the result equals the fp64 sequential-sum definition except where a running
 // sum lies within about 1e-6 of p.
@@ -33,7 +33,7 @@ namespace {
 
 constexpr int kPoolThreads = 512;  // one wavefront per block, 8 blocks
 constexpr int kSelRows = 16;         // query blocks per select workgroup
-constexpr double kMassScale = 4611686018427387904.0;  // 2^62
+constexpr double kMassScale = 4503599627370496.0;  // 2^52
 
 // Pooled means are stored in the operand order of the fp64 16x16x4 MFMA of
 // select_kernel: per head, tiles of 16 blocks; within tile T, load step u
@@ -51,6 +51,19 @@ constexpr int kPoolBlocks = 8;  // blocks per pool workgroup (half an operand ti
 // 256-byte token rows), the four slots are summed across lanes, and the
 // means are staged in operand order; the group's 16 KB of Q and K means are
 // then written as whole lines.
+// x[l] + x[l^16] + x[l^32] + x[l^48] in every lane, with the lane-swap
+// instructions (both partners add the same two operands).
+__device__ __forceinline__ double sum_rows4(double v) {
+  uint64_t b = (uint64_t)__double_as_longlong(v);
+  auto lo = __builtin_amdgcn_permlane16_swap((uint32_t)b, (uint32_t)b, false, false);
+  auto hi = __builtin_amdgcn_permlane16_swap((uint32_t)(b >> 32), (uint32_t)(b >> 32), false, false);
+  v = __longlong_as_double((long long)join64(lo[0], hi[0])) + __longlong_as_double((long long)join64(lo[1], hi[1]));
+  b = (uint64_t)__double_as_longlong(v);
+  lo = __builtin_amdgcn_permlane32_swap((uint32_t)b, (uint32_t)b, false, false);
+  hi = __builtin_amdgcn_permlane32_swap((uint32_t)(b >> 32), (uint32_t)(b >> 32), false, false);
+  return __longlong_as_double((long long)join64(lo[0], hi[0])) + __longlong_as_double((long long)join64(lo[1], hi[1]));
+}
+
 constexpr int kPoolRowsPerStep = 16;  // token rows each lane loads per step
 static_assert(kPoolThreads == 64 * kPoolBlocks, "one wavefront per pooled block");
 __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __restrict__ Q,
@@ -115,10 +128,8 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
   // Sum the four slots: lanes c, c + 16, c + 32, c + 48.
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    aq[e] += __shfl_xor(aq[e], 16);
-    ak[e] += __shfl_xor(ak[e], 16);
-    aq[e] += __shfl_xor(aq[e], 32);
-    ak[e] += __shfl_xor(ak[e], 32);
+    aq[e] = sum_rows4(aq[e]);
+    ak[e] = sum_rows4(ak[e]);
   }
   // Slot 0 stores the Q means, slot 1 the K means (zero for padding blocks):
   // dims 8c + 2v, 8c + 2v + 1 are pair (u, g) = (4 (c % 4) + v, c / 4).
@@ -157,24 +168,38 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
 // with the hardware exp2 in fp32: relative error below 2^-21, far inside
 // what the Top-p decision needs (the scores themselves, which decide the
 // order, stay fp64). Masses below 2^-126 flush to zero; they are below the
-// 2^-62 quantum of the fixed-point sums anyway.
+// 2^-52 quantum of the fixed-point sums anyway.
 __device__ __forceinline__ double block_exp(double s, double smax) {
   return (double)__builtin_amdgcn_exp2f((float)((s - smax) * 1.4426950408889634));
 }
 
-// Fixed-point mass of one block: round(block_exp(s, smax) * (2^62 / Z)).
-// Every caller evaluates exactly this expression, so a block's mass is the
-// same wherever it is recomputed.
-__device__ __forceinline__ uint64_t block_mass(double s, double smax, double zs) {
-  return (uint64_t)__double2ull_rn(__dmul_rn(block_exp(s, smax), zs));
+// Nearest integer (ties to even) of x in [0, 2^52]: x + 2^52 rounds to an
+// integer, and its bit pattern exceeds that of 2^52 by exactly that integer
+// (also for x = 2^52, where the exponent steps up by one).
+__device__ __forceinline__ uint64_t round_mass(double x) {
+  return (uint64_t)__double_as_longlong(__dadd_rn(x, kMassScale)) - (uint64_t)__double_as_longlong(kMassScale);
 }
 
+// Fixed-point mass of one block: round(block_exp(s, smax) * (2^52 / Z)).
+// Z >= 1 (it holds the maximum's exp(0) = 1), so the product is at most
+// 2^52. Every caller evaluates exactly this expression, so a block's mass is
+// the same wherever it is recomputed.
+__device__ __forceinline__ uint64_t block_mass(double s, double smax, double zs) {
+  return round_mass(__dmul_rn(block_exp(s, smax), zs));
+}
+
+// A bucket of the radix select holds (count << 53) + summed weight in one
+// 64-bit word: weights of a row sum to at most 2^52 + nb / 2 < 2^53, and
+// counts to at most 1024, so one atomic add and one scan carry both.
+constexpr uint64_t kOneCount = 1ull << 53;
+constexpr uint64_t kWeightBits = kOneCount - 1;
+
 struct WaveScratch {
-  uint32_t cnt[64];
-  uint64_t wt[64];
-  int list_j[64];
-  int slot_j[64];
-  uint64_t slot_w[64];
+  uint64_t hist[64];  // packed bucket words
+  double cs[64];      // candidates: score, weight, block id
+  uint64_t cw[64];
+  int cj[64];
+  uint64_t kept[16];  // kept-block bits of the row, 64 blocks per word
 };
 
 struct Cut {
@@ -186,18 +211,19 @@ struct Cut {
 // Finds the block q at which the running weight (fixed-point mass, or 1 per
 // block when by_mass is false) first reaches thr, walking blocks in
 // (score desc, id asc) order. Requires thr >= 1 and total weight >= thr.
+// Each level buckets the candidates by score into 64 buckets (bucket 0 for
+// the highest scores), scans the bucket words and keeps only the bucket in
+// which the running weight crosses thr; once at most 64 candidates remain,
+// every candidate sums the weights of those that precede it.
 template <int KPL>
-__device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL], const uint64_t (&F)[KPL],
-                          uint32_t valid, double smin, double smax, double zs, bool by_mass, uint64_t thr,
-                          WaveScratch& ws, int lane) {
+__device__ Cut select_cut(const double (&s)[KPL], const uint64_t (&F)[KPL], uint32_t valid, int nvalid, double smin,
+                          double smax, double zs, bool by_mass, uint64_t thr, WaveScratch& ws, int lane) {
   uint32_t cand = valid;
-  uint64_t W0 = 0;
-  int C0 = 0;
+  int ncand = nvalid;
+  uint64_t W0 = 0;  // weight of the blocks ahead of every candidate
+  int C0 = 0;       // their number
   double lo = smin, hi = smax;
   for (int level = 0; level < 2 * kMaxBlocks; ++level) {  // each level drops >= 1 candidate
-    int ncand = 0;
-#pragma unroll
-    for (int k = 0; k < KPL; ++k) ncand += __popcll(__ballot((cand >> k) & 1u));
     if (ncand <= 64 || !(hi > lo)) {
       // Gather the candidates in ascending block id order.
       int base = 0;
@@ -205,14 +231,16 @@ __device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL
       for (int k = 0; k < KPL; ++k) {
         const bool is = (cand >> k) & 1u;
         const uint64_t m = __ballot(is);
-        if (is) {
-          const int pos = base + lanes_below(m);
-          if (pos < 64) ws.list_j[pos] = lane + 64 * k;
+        const int pos = base + lanes_below(m);
+        if (is && pos < 64) {
+          ws.cs[pos] = s[k];
+          ws.cj[pos] = lane + 64 * k;
+          ws.cw[pos] = by_mass ? F[k] : 1ull;
         }
         base += __popcll(m);
       }
       wave_sync();
-      if (!(hi > lo) && ncand > 64) {
+      if (ncand > 64) {
         // Every candidate has the same score: they follow in id order, each
         // with the same weight, so the cut is the t-th smallest id.
         const uint64_t w = by_mass ? block_mass(hi, smax, zs) : 1ull;
@@ -229,89 +257,84 @@ __device__ Cut select_cut(const double* __restrict__ srow, const double (&s)[KPL
           const int cntk = __popcll(m);
           if (cut_j < 0 && seen + cntk >= (int)t) {
             const int want = (int)t - seen;  // 1-based within this k
-            if (is && lanes_below(m) + 1 == want) ws.list_j[0] = lane + 64 * k;
-            wave_sync();
-            cut_j = ws.list_j[0];
+            const uint64_t at = __ballot(is && lanes_below(m) + 1 == want);
+            cut_j = 64 * k + __ffsll((unsigned long long)at) - 1;
           }
           seen += cntk;
         }
         Cut c;
         c.j = cut_j;
-        c.s = srow[cut_j];
+        c.s = hi;
         c.rank = C0 + (int)t;
         return c;
       }
-      // At most 64 candidates: rank them exactly. Candidate m's score and
-      // id are broadcast from lane m with readlane (no memory round trips).
+      // At most 64 candidates, one per lane: each sums the weights of the
+      // candidates ahead of it (read as LDS broadcasts), so the crossing is
+      // the one candidate with before < thr <= before + own weight.
       const bool has = lane < ncand;
-      const int jl = has ? ws.list_j[lane] : 0;
-      const double sl = srow[jl];
+      const double sl = has ? ws.cs[lane] : 0.0;
+      const int jl = has ? ws.cj[lane] : 0;
+      const uint64_t wl = has ? ws.cw[lane] : 0ull;
+      uint64_t ahead = 0;
       int rank = 0;
-      for (int m = 0; m < ncand; ++m) {  // ncand <= 64 here
-        const int jm = __builtin_amdgcn_readlane(jl, m);
-        const double sm = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(sl), m),
-                                           __builtin_amdgcn_readlane(__double2loint(sl), m));
-        rank += (sm > sl || (sm == sl && jm < jl)) ? 1 : 0;
+#pragma unroll 4
+      for (int m = 0; m < ncand; ++m) {
+        const double sm = ws.cs[m];
+        const int jm = ws.cj[m];
+        const bool prec = sm > sl || (sm == sl && jm < jl);
+        ahead += prec ? ws.cw[m] : 0ull;
+        rank += prec ? 1 : 0;
       }
-      const uint64_t wl = has ? (by_mass ? block_mass(sl, smax, zs) : 1ull) : 0ull;
-      wave_sync();
-      if (has && rank < 64) {
-        ws.slot_j[rank] = jl;
-        ws.slot_w[rank] = wl;
-      }
-      wave_sync();
-      const uint64_t myw = has ? ws.slot_w[lane] : 0ull;
-      const uint64_t cum = W0 + wave_incl_scan_u64(myw, lane);
-      const uint64_t hit = __ballot(has && cum >= thr);
-      int pos = hit ? (__ffsll((unsigned long long)hit) - 1) : (ncand - 1);
+      const uint64_t before = W0 + ahead;
+      uint64_t hit = __ballot(has && before < thr && before + wl >= thr);
+      if (!hit) hit = __ballot(has && rank == ncand - 1);  // not reached: thr is within the total
+      const int pos = __ffsll((unsigned long long)hit) - 1;
       Cut c;
-      c.j = ws.slot_j[pos];
-      c.s = srow[c.j];
-      c.rank = C0 + pos + 1;
+      c.j = __builtin_amdgcn_readlane(jl, pos);
+      c.s = __longlong_as_double((long long)lane_u64((uint64_t)__double_as_longlong(sl), pos));
+      c.rank = C0 + __builtin_amdgcn_readlane(rank, pos) + 1;
       wave_sync();
       return c;
     }
-    // Bucket the candidates by score, highest scores in bucket 0: the bucket
-    // floor((hi - s) * 64 / (hi - lo)) is non-decreasing as s falls.
-    ws.cnt[lane] = 0u;
-    ws.wt[lane] = 0ull;
+    // Bucket floor((hi - s) * 64 / (hi - lo)) is non-decreasing as s falls;
+    // any positive scale keeps that order, so it need not be exact.
+    ws.hist[lane] = 0ull;
     wave_sync();
-    const double scale = __ddiv_rn(64.0, hi - lo);
+    const double scale = 64.0 / (hi - lo);
+    int bk[KPL];
 #pragma unroll
     for (int k = 0; k < KPL; ++k) {
-      if ((cand >> k) & 1u) {
-        int bkt = (int)__dmul_rn(hi - s[k], scale);
-        bkt = bkt < 0 ? 0 : (bkt > 63 ? 63 : bkt);
-        atomicAdd(&ws.cnt[bkt], 1u);
-        atomicAdd((unsigned long long*)&ws.wt[bkt], (unsigned long long)(by_mass ? F[k] : 1ull));
-      }
+      const bool is = (cand >> k) & 1u;
+      int b = (int)__dmul_rn(hi - s[k], scale);
+      b = b < 0 ? 0 : (b > 63 ? 63 : b);
+      bk[k] = b;
+      // Lanes without a candidate add 0 to their own word: no branch and no
+      // address conflict.
+      atomicAdd((unsigned long long*)&ws.hist[is ? b : lane],
+                (unsigned long long)(is ? kOneCount + (by_mass ? F[k] : 1ull) : 0ull));
     }
     wave_sync();
-    const uint64_t wb = ws.wt[lane];
-    const int cb = (int)ws.cnt[lane];
-    const uint64_t cumw = W0 + wave_incl_scan_u64(wb, lane);
-    const int cumc = wave_incl_scan_i32(cb, lane);
-    const uint64_t hit = __ballot(cumw >= thr);
+    const uint64_t hv = ws.hist[lane];
+    const uint64_t inc = wave_incl_scan_u64(hv, lane);
+    const uint64_t hit = __ballot(W0 + (inc & kWeightBits) >= thr);
     const int bstar = hit ? (__ffsll((unsigned long long)hit) - 1) : 63;
-    W0 = __shfl(cumw - wb, bstar);
-    C0 += __shfl(cumc - cb, bstar);
+    const uint64_t ahead = lane_u64(inc - hv, bstar);
+    W0 += ahead & kWeightBits;
+    C0 += (int)(ahead >> 53);
+    ncand = (int)(lane_u64(hv, bstar) >> 53);
     wave_sync();
     double nlo = 1.0e308, nhi = -1.0e308;
 #pragma unroll
     for (int k = 0; k < KPL; ++k) {
-      if ((cand >> k) & 1u) {
-        int bkt = (int)__dmul_rn(hi - s[k], scale);
-        bkt = bkt < 0 ? 0 : (bkt > 63 ? 63 : bkt);
-        if (bkt != bstar) {
-          cand &= ~(1u << k);
-        } else {
-          nlo = fmin(nlo, s[k]);
-          nhi = fmax(nhi, s[k]);
-        }
-      }
+      const bool keep = ((cand >> k) & 1u) && bk[k] == bstar;
+      cand = keep ? cand : (cand & ~(1u << k));
+      nlo = keep ? fmin(nlo, s[k]) : nlo;
+      nhi = keep ? fmax(nhi, s[k]) : nhi;
     }
-    lo = wave_min(nlo);
-    hi = wave_max(nhi);
+    if (ncand > 64) {
+      lo = wave_min(nlo);
+      hi = wave_max(nhi);
+    }
   }
   // Not reached for finite scores; keep every block as a safe fallback.
   Cut c;
@@ -357,7 +380,7 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
   uint64_t tot = 0;
 #pragma unroll
   for (int k = 0; k < KPL; ++k) {
-    F[k] = ((valid >> k) & 1u) ? (uint64_t)__double2ull_rn(__dmul_rn(__longlong_as_double((long long)F[k]), zs)) : 0ull;
+    F[k] = ((valid >> k) & 1u) ? round_mass(__dmul_rn(__longlong_as_double((long long)F[k]), zs)) : 0ull;
     tot += F[k];
   }
   const uint64_t total = wave_sum_u64(tot);
@@ -377,13 +400,16 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
     } else if (total < T) {
       m_p = nb;
     } else {
-      cut = select_cut<KPL>(srow, s, F, valid, smin, smax, zs, true, T, ws, lane);
+      cut = select_cut<KPL>(s, F, valid, nb, smin, smax, zs, true, T, ws, lane);
       m_p = cut.rank;
     }
   }
   const int m = m_p > kf ? m_p : kf;
-  if (m > 0 && m < nb && m != m_p) cut = select_cut<KPL>(srow, s, F, valid, smin, smax, zs, false, (uint64_t)m, ws, lane);
+  if (m > 0 && m < nb && m != m_p) cut = select_cut<KPL>(s, F, valid, nb, smin, smax, zs, false, (uint64_t)m, ws, lane);
 
+  // Kept blocks: the first m of (score desc, id asc), i.e. those ahead of or
+  // equal to the cut block.
+  uint64_t mine = 0;  // lane k < KPL holds the kept bits of blocks 64k .. 64k+63
   int base = 0;
 #pragma unroll
   for (int k = 0; k < KPL; ++k) {
@@ -393,37 +419,63 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
     else if (m >= nb) kept = true;
     else kept = (s[k] > cut.s) || (s[k] == cut.s && j <= cut.j);
     kept = kept && (j < nb);
-    if (j < nb) mrow[j] = kept ? 1 : 0;
     const uint64_t bal = __ballot(kept);
+    mine = lane == k ? bal : mine;
     if (kvrow && kept) kvrow[base + lanes_below(bal)] = j;
     base += __popcll(bal);
+  }
+  if ((nb & 3) == 0 && (reinterpret_cast<uintptr_t>(mrow) & 3) == 0) {
+    // 4-byte aligned row of whole words: lane L writes bytes 4w .. 4w+3,
+    // w = L + 64i, expanding four kept bits into four 0/1 bytes.
+    if (lane < KPL) ws.kept[lane] = mine;
+    wave_sync();
+    uint32_t* mw = reinterpret_cast<uint32_t*>(mrow);
+    for (int w = lane; 4 * w < nb; w += 64) {
+      const uint32_t nib = (uint32_t)(ws.kept[w >> 4] >> (4 * (w & 15))) & 0xFu;
+      mw[w] = (nib * 0x204081u) & 0x01010101u;
+    }
+    wave_sync();
+  } else {
+#pragma unroll
+    for (int k = 0; k < KPL; ++k) {
+      const int j = lane + 64 * k;
+      const uint64_t bal = __builtin_amdgcn_readlane((uint32_t)mine, k) |
+                           ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(mine >> 32), k) << 32);
+      if (j < nb) mrow[j] = (bal >> lane) & 1u;
+    }
   }
   if (lane == 0) *count_out = m;
 }
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
-constexpr int kSelThreads = 512;  // 8 waves
+constexpr int kScoreThreads = 512;  // 8 waves
+constexpr int kRowWaves = 4;        // rows (one per wavefront) per select workgroup
 
-// Scores of 16 query blocks against every key block with the fp64 MFMA
-// (16x16x4): lane (row l%16, group g = l/16) feeds dim 32g + k of its query
-// row and its key at step k, so the 32 steps sum the full 128-dim dot
-// product. Wave w takes key tiles w, w+8, ...; then each wave selects rows w
-// and w+8.
-template <int KPL>
-__global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __restrict__ qbar,
-                                                                const double* __restrict__ kbar, int nb, double p,
-                                                                int k_min, uint8_t* __restrict__ mask,
-                                                                int32_t* __restrict__ counts,
-                                                                int32_t* __restrict__ kv_idx) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  double* sc = reinterpret_cast<double*>(smem);  // [kSelRows][nb]
-  WaveScratch* wsa = reinterpret_cast<WaveScratch*>(smem + sizeof(double) * kSelRows * nb);
-  const int bh = blockIdx.y;
-  const int i0 = blockIdx.x * kSelRows;
-  const int rows = min(kSelRows, nb - i0);
+// Workgroup n of a 1-D grid runs on XCD n % 8. Logical workgroups are dealt
+// out so that each XCD takes one contiguous run of them: the query tiles of
+// whole heads, whose pooled keys then stay in that XCD's L2.
+__device__ __forceinline__ int xcd_contiguous(int n, int total) {
+  const int q = total >> 3, r = total & 7, x = n & 7;
+  return x * q + min(x, r) + (n >> 3);
+}
+
+// Scores s_ij = qbar_i . kbar_j / sqrt(128) of 16 query blocks against every
+// key block with the fp64 MFMA (16x16x4): lane (row l%16, group g = l/16)
+// feeds dim 32g + k of its query row and its key at step k, so the 32 steps
+// sum the full 128-dim dot product. Wave w takes key tiles w, w+8, ... The
+// grid is one-dimensional over (head, query tile); scores go to a row-major
+// [B*H*nb, nb] fp64 buffer.
+__global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __restrict__ qbar,
+                                                             const double* __restrict__ kbar, int nb,
+                                                             double* __restrict__ scores) {
+  const int ntq = (nb + kSelRows - 1) / kSelRows;
+  const int L = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int bh = L / ntq;
+  const int tq = L - bh * ntq;  // query tile
+  const int i0 = tq * kSelRows;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nwaves = kSelThreads / 64;
+  const int nwaves = kScoreThreads / 64;
   const int m16 = lane & 15;
   const int g = lane >> 4;
   const double inv_sqrt_d = 11.313708498984761;  // sqrt(128): s = dot / sqrt(128)
@@ -436,7 +488,7 @@ __global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __
   const int64_t head_off = (int64_t)bh * padded_blocks(nb) * kHeadDim;
   double qa[32];
   {
-    const double* qr = qbar + head_off + (int64_t)blockIdx.x * 16 * kHeadDim + 2 * lane;
+    const double* qr = qbar + head_off + (int64_t)tq * 16 * kHeadDim + 2 * lane;
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const double2 v = *reinterpret_cast<const double2*>(qr + u * 128);
@@ -445,6 +497,7 @@ __global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __
     }
   }
   const double* kb = kbar + head_off + 2 * lane;
+  double* srow = scores + ((int64_t)bh * nb + i0) * nb;
   // Key tile t's operands load while tile t - 8 multiplies.
   auto load_tile = [&](int t, double (&kk)[32]) {
     const double* kr = kb + (int64_t)t * 16 * kHeadDim;
@@ -460,11 +513,14 @@ __global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __
 #pragma unroll
     for (int k = 0; k < 32; ++k) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[k], kk[k], acc, 0, 0, 0);
     // D layout of the fp64 16x16x4 MFMA: lane holds rows g + 4e (e = 0..3)
-    // of key column m16.
+    // of key column m16; sixteen lanes store 128 contiguous bytes of a row.
     const int key = t * 16 + m16;
     if (key < nb) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sc[(g + 4 * e) * nb + key] = __ddiv_rn(acc[e], inv_sqrt_d);
+      for (int e = 0; e < 4; ++e) {
+        const int r = g + 4 * e;
+        if (i0 + r < nb) srow[(int64_t)r * nb + key] = __ddiv_rn(acc[e], inv_sqrt_d);
+      }
     }
   };
   double ka[32], kn[32];
@@ -481,38 +537,51 @@ __global__ __launch_bounds__(kSelThreads, 1) void select_kernel(const double* __
     score_tile(t, kn);
     t = tn2;
   }
-  __syncthreads();
+}
 
-  for (int r = wave; r < rows; r += nwaves) {
-    const int64_t row = (int64_t)bh * nb + i0 + r;
-    select_row<KPL>(sc + r * nb, nb, p, k_min, mask + row * nb, counts + row, kv_idx ? kv_idx + row * nb : nullptr,
-                    wsa[wave], lane);
-  }
+// Top-p / Top-k selection of one score row per wavefront.
+template <int KPL>
+__global__ __launch_bounds__(64 * kRowWaves, KPL > 12 ? 3 : 4) void select_kernel(const double* __restrict__ scores, int nb,
+                                                                   int64_t nrows, double p, int k_min,
+                                                                   uint8_t* __restrict__ mask,
+                                                                   int32_t* __restrict__ counts,
+                                                                   int32_t* __restrict__ kv_idx) {
+  __shared__ WaveScratch wsa[kRowWaves];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t row = (int64_t)blockIdx.x * kRowWaves + wave;
+  if (row >= nrows) return;
+  select_row<KPL>(scores + row * nb, nb, p, k_min, mask + row * nb, counts + row, kv_idx ? kv_idx + row * nb : nullptr,
+                  wsa[wave], lane);
 }
 
 template <int KPL>
-hipError_t launch_select(const RouteArgs& a, int nb, double* qbar, double* kbar) {
-  const int bhs = a.batch * a.heads;
-  const size_t lds = sizeof(double) * kSelRows * nb + sizeof(WaveScratch) * (kSelThreads / 64);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<KPL>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  dim3 grid((nb + kSelRows - 1) / kSelRows, bhs);
-  hipLaunchKernelGGL(select_kernel<KPL>, grid, dim3(kSelThreads), lds, a.stream, qbar, kbar, nb, a.p, a.k_min, a.mask,
-                     a.counts, a.kv_idx);
+hipError_t launch_select(const RouteArgs& a, int nb, const double* scores) {
+  const int64_t nrows = (int64_t)a.batch * a.heads * nb;
+  const dim3 grid((unsigned)((nrows + kRowWaves - 1) / kRowWaves));
+  hipLaunchKernelGGL(select_kernel<KPL>, grid, dim3(64 * kRowWaves), 0, a.stream, scores, nb, nrows, a.p, a.k_min,
+                     a.mask, a.counts, a.kv_idx);
   return hipGetLastError();
+}
+
+// Workspace: pooled Q means, pooled K means (operand order, blocks padded to
+// 16), then the fp64 score rows; each part 256-byte aligned.
+struct RouteWorkspace {
+  size_t means;   // bytes of one means array
+  size_t scores;  // bytes of the score rows
+};
+RouteWorkspace route_workspace_parts(int batch, int heads, int nb) {
+  RouteWorkspace w;
+  w.means = ((size_t)batch * heads * padded_blocks(nb) * kHeadDim * sizeof(double) + 255) & ~(size_t)255;
+  w.scores = ((size_t)batch * heads * nb * nb * sizeof(double) + 255) & ~(size_t)255;
+  return w;
 }
 
 }  // namespace
 
 size_t route_workspace_bytes(int batch, int heads, int nb) {
-  const size_t one = (size_t)batch * heads * padded_blocks(nb) * kHeadDim * sizeof(double);
-  const size_t aligned = (one + 255) & ~(size_t)255;
-  return 2 * aligned;
+  const RouteWorkspace w = route_workspace_parts(batch, heads, nb);
+  return 2 * w.means + w.scores;
 }
 
 hipError_t launch_route(const RouteArgs& a) {
@@ -520,20 +589,26 @@ hipError_t launch_route(const RouteArgs& a) {
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
   const int bhs = a.batch * a.heads;
   if (bhs == 0) return hipSuccess;
-  const size_t one = ((size_t)bhs * padded_blocks(g.nb) * kHeadDim * sizeof(double) + 255) & ~(size_t)255;
-  double* qbar = reinterpret_cast<double*>(a.workspace);
-  double* kbar = reinterpret_cast<double*>(reinterpret_cast<char*>(a.workspace) + one);
+  const RouteWorkspace w = route_workspace_parts(a.batch, a.heads, g.nb);
+  char* base = reinterpret_cast<char*>(a.workspace);
+  double* qbar = reinterpret_cast<double*>(base);
+  double* kbar = reinterpret_cast<double*>(base + w.means);
+  double* scores = reinterpret_cast<double*>(base + 2 * w.means);
   hipLaunchKernelGGL(pool_kernel, dim3(padded_blocks(g.nb) / kPoolBlocks, bhs), dim3(kPoolThreads), 0, a.stream,
                      reinterpret_cast<const uint16_t*>(a.Q), reinterpret_cast<const uint16_t*>(a.K), a.heads,
                      a.stride_b, a.stride_h, a.stride_n, g, qbar, kbar);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(score_kernel, dim3((g.nb + kSelRows - 1) / kSelRows * bhs), dim3(kScoreThreads), 0, a.stream,
+                     qbar, kbar, g.nb, scores);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const int kpl = (g.nb + 63) / 64;
-  if (kpl <= 2) return launch_select<2>(a, g.nb, qbar, kbar);
-  if (kpl <= 4) return launch_select<4>(a, g.nb, qbar, kbar);
-  if (kpl <= 8) return launch_select<8>(a, g.nb, qbar, kbar);
-  if (kpl <= 12) return launch_select<12>(a, g.nb, qbar, kbar);
-  return launch_select<16>(a, g.nb, qbar, kbar);
+  if (kpl <= 2) return launch_select<2>(a, g.nb, scores);
+  if (kpl <= 4) return launch_select<4>(a, g.nb, scores);
+  if (kpl <= 8) return launch_select<8>(a, g.nb, scores);
+  if (kpl <= 12) return launch_select<12>(a, g.nb, scores);
+  return launch_select<16>(a, g.nb, scores);
 }
 
 }  // namespace fva

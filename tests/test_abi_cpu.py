@@ -53,8 +53,9 @@ T720 = fva.Tiling(21, 45, 80, 2, 8, 8)
 def test_workspace_sizes():
     nb = 660
     rows = 40 * nb
-    # fp64 means of Q and K, blocks padded to a multiple of 16 (660 -> 672)
-    assert fva.fva_route_workspace_size(desc(), T720) == 2 * 40 * 672 * 128 * 8
+    # fp64 means of Q and K, blocks padded to a multiple of 16 (660 -> 672),
+    # then the fp64 score rows
+    assert fva.fva_route_workspace_size(desc(), T720) == 2 * 40 * 672 * 128 * 8 + 40 * nb * nb * 8
     al = lambda x: (x + 255) // 256 * 256
     # counts, kept lists, queue items, 9 queue bases, 8 queue counters, per-head plan scratch
     heads = 40
