@@ -144,9 +144,6 @@ __device__ __forceinline__ void row_offsets(const AttnParams& P, const BlockMap&
 // Asynchronous global -> LDS copy of this wave's 8 KB of a tile. K rows use a
 // 16-byte-chunk XOR swizzle (chunk ^ row%16), V rows an 8-byte-chunk swizzle
 // (chunk8 ^ 4*(row%8)); both make the MFMA-side reads bank-conflict free.
-// Asynchronous global -> LDS copy of this wave's 8 KB of a tile. K rows use a
-// 16-byte-chunk XOR swizzle (chunk ^ row%16), V rows an 8-byte-chunk swizzle
-// (chunk8 ^ 4*(row%8)); both make the MFMA-side reads bank-conflict free.
 // The copies are issued from inline assembly so that the compiler does not
 // drain them (vmcnt(0)) before unrelated LDS reads; the kernel waits for them
 // explicitly (wait_vmem) before the barrier that publishes a tile. M0 holds
@@ -316,6 +313,9 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         bf16x8 kq[kKPre + 1];
 #pragma unroll
         for (int u = 0; u < kKPre; ++u) kq[u] = kfrag(4 * hb + (u >> 2), u & 3);
+        // Issue priority while multiplying: the SIMD's other wave (another
+        // workgroup, usually in its softmax) fills the matrix unit's gaps.
+        __builtin_amdgcn_s_setprio(2);
 #pragma unroll
         for (int u = 0; u < 16; ++u) {
           const int t = u >> 2, ks = u & 3;
@@ -326,6 +326,7 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
           s[t][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[1][ks], ks == 0 ? z : s[t][1], 0, 0, 0);
           __builtin_amdgcn_sched_barrier(0);
         }
+        __builtin_amdgcn_s_setprio(0);
       }
       if (hb == 1) {
         tile_barrier();  // every wave is done with K_c
@@ -429,6 +430,7 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         bf16x8 vq[kVPre + 1];
 #pragma unroll
         for (int u = 0; u < kVPre; ++u) vq[u] = vfrag(2 * hb + (u >> 3), u & 7);
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int u = 0; u < 16; ++u) {
           const int kk = u >> 3, mt = u & 7;
@@ -442,6 +444,7 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
           }
           __builtin_amdgcn_sched_barrier(0);
         }
+        __builtin_amdgcn_s_setprio(0);
       }
     }
     tile_barrier();  // every wave is done with V_c
