@@ -57,9 +57,13 @@ def real_pairs(mask, sizes):
     return float(np.einsum("hij,i,j->", m, n, n))
 
 
-def source_digest(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def source_digest(*paths):
+    """Digest of a kernel source and the headers it shares with the others."""
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def imbalance(trace, counts):
@@ -143,9 +147,11 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0):
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each scaled by the factor the same
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
-ATTN_TRAFFIC = {"source_digest": "dc73de173e08185e", "workload": "720p", "bytes": 235912492093 + 775236160}
-# Same for fva_route (pool_kernel + select_kernel), per call on the 720p workload.
-ROUTE_TRAFFIC = {"source_digest": "b4d21ba48bd95b23", "workload": "720p", "bytes": (756006 + 126133) * 2048 + (52800 + 49132) * 1024}
+ATTN_TRAFFIC = {"source_digest": "a094367503c3a30f", "workload": "720p", "bytes": (114126688 * 2 + 757084) * 1024}
+# Same for fva_route (pool_kernel + score_kernel + select_kernel), per call on
+# the 720p workload (FETCH x 2, WRITE x 1, KiB per dispatch summed).
+ROUTE_TRAFFIC = {"source_digest": "7d143e4920346349", "workload": "720p",
+                 "bytes": ((756185 + 29354 + 68211) * 2 + 53760 + 138225 + 49287) * 1024}
 
 
 def copy_calibration(torch, gib=1.0, reps=5):
@@ -260,11 +266,13 @@ def main():
     dense_flops = 4.0 * B * H * float(N) ** 2 * d
     route_bytes = 2.0 * B * H * N * d * 2 + B * H * nb * nb + 4.0 * B * H * nb + 4.0 * kept
     here = os.path.dirname(os.path.abspath(__file__))
-    digest = source_digest(os.path.join(here, "paper_2607_16190_amd", "csrc", "attn_kernels.hip"))
+    csrc = os.path.join(here, "paper_2607_16190_amd", "csrc")
+    shared = [os.path.join(csrc, f) for f in ("fva_common.h", "fva_geometry.h")]
+    digest = source_digest(os.path.join(csrc, "attn_kernels.hip"), *shared)
     traffic = None
     if ATTN_TRAFFIC["source_digest"] == digest and ATTN_TRAFFIC["workload"] == cfg.name and args.sched == "persistent":
         traffic = ATTN_TRAFFIC["bytes"]
-    route_digest = source_digest(os.path.join(here, "paper_2607_16190_amd", "csrc", "route_kernels.hip"))
+    route_digest = source_digest(os.path.join(csrc, "route_kernels.hip"), *shared)
     route_traffic = None
     if ROUTE_TRAFFIC["source_digest"] == route_digest and ROUTE_TRAFFIC["workload"] == cfg.name:
         route_traffic = ROUTE_TRAFFIC["bytes"]

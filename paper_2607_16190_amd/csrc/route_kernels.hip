@@ -448,7 +448,7 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
 }
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
-constexpr int kScoreThreads = 512;  // 8 waves
+constexpr int kScoreThreads = 256;  // 4 waves; two workgroups per CU overlap their start-up loads
 constexpr int kRowWaves = 4;        // rows (one per wavefront) per select workgroup
 
 // Workgroup n of a 1-D grid runs on XCD n % 8. Logical workgroups are dealt
@@ -462,7 +462,7 @@ __device__ __forceinline__ int xcd_contiguous(int n, int total) {
 // Scores s_ij = qbar_i . kbar_j / sqrt(128) of 16 query blocks against every
 // key block with the fp64 MFMA (16x16x4): lane (row l%16, group g = l/16)
 // feeds dim 32g + k of its query row and its key at step k, so the 32 steps
-// sum the full 128-dim dot product. Wave w takes key tiles w, w+8, ... The
+// sum the full 128-dim dot product. Wave w takes key tiles w, w+4, ... The
 // grid is one-dimensional over (head, query tile); scores go to a row-major
 // [B*H*nb, nb] fp64 buffer.
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __restrict__ qbar,
@@ -498,7 +498,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __re
   }
   const double* kb = kbar + head_off + 2 * lane;
   double* srow = scores + ((int64_t)bh * nb + i0) * nb;
-  // Key tile t's operands load while tile t - 8 multiplies.
+  // A wave's next key tile loads while its current one multiplies.
   auto load_tile = [&](int t, double (&kk)[32]) {
     const double* kr = kb + (int64_t)t * 16 * kHeadDim;
 #pragma unroll
