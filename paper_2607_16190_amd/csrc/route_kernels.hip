@@ -439,8 +439,7 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
 #pragma unroll
     for (int k = 0; k < KPL; ++k) {
       const int j = lane + 64 * k;
-      const uint64_t bal = __builtin_amdgcn_readlane((uint32_t)mine, k) |
-                           ((uint64_t)__builtin_amdgcn_readlane((uint32_t)(mine >> 32), k) << 32);
+      const uint64_t bal = lane_u64(mine, k);
       if (j < nb) mrow[j] = (bal >> lane) & 1u;
     }
   }

@@ -75,6 +75,7 @@ PARTIAL = [
     ((3, 9, 10), (1, 8, 8)),
     ((4, 32, 40), (1, 8, 8)),  # nb = 80 > 64: several lanes per row
     ((7, 17, 29), (2, 8, 8)),
+    ((5, 24, 40), (1, 8, 8)),  # nb = 75: rows not whole words, blocks past 32 in each 64
 ]
 
 
@@ -142,3 +143,54 @@ def test_route_batch_two_odd_heads():
     Qb, Kb, _ = synth.gen_qkv(cfg)
     assert Qb.shape[:2] == (2, 3)
     check_route("batch2", Qb, Kb, cfg, cfg.p, cfg.k_min)
+
+
+def test_route_unaligned_mask_rows():
+    # Mask rows of whole 32-bit words go out as words only when the row start
+    # is 4-byte aligned; a mask at an odd address takes the byte stores.
+    # Both must give the same mask (nb = 80, a multiple of 4).
+    cfg = custom_config("unaligned", 3, (4, 32, 40), (1, 8, 8), (0.7, 2.0, 4.0), seed=21)
+    nb = geometry_of(cfg).nb
+    assert nb % 4 == 0
+    Qb, Kb, _ = synth.gen_qkv(cfg)
+    mask, counts, kv = gpu_route(Qb, Kb, cfg, cfg.p, cfg.k_min)
+    fva, torch = lib(), torch_mod()
+    q, k = to_dev(Qb), to_dev(Kb)
+    for offset in (1, 2, 3):
+        buf = torch.zeros(mask.size + 4, dtype=torch.uint8, device="cuda:0")
+        m_dev = buf[offset:offset + mask.size].view(mask.shape)
+        c_dev = torch.empty(counts.shape, dtype=torch.int32, device="cuda:0")
+        k_dev = torch.empty(kv.shape, dtype=torch.int32, device="cuda:0")
+        fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg), out=(m_dev, c_dev, k_dev))
+        torch.cuda.synchronize()
+        assert np.array_equal(m_dev.cpu().numpy(), mask), offset
+        assert np.array_equal(c_dev.cpu().numpy(), counts), offset
+        host = buf.cpu().numpy()
+        assert not host[:offset].any() and not host[offset + mask.size:].any(), offset  # nothing outside the view
+    check_route("unaligned", Qb, Kb, cfg, cfg.p, cfg.k_min)
+
+
+def test_route_multilevel_select():
+    # One key block far below the rest stretches the score range, so the
+    # first 64-bucket pass leaves the whole cluster (~150 blocks) in the
+    # bucket where the running mass crosses p and the radix select takes a
+    # second level before ranking. nb = 300.
+    grid, tile = (10, 40, 48), (1, 8, 8)
+    cfg = custom_config("multilevel", 1, grid, tile, (1.0,), seed=5)
+    geo = geometry_of(cfg)
+    T, H, W = grid
+    rng = np.random.default_rng(5)
+    u = rng.standard_normal(128)
+    u /= np.linalg.norm(u)
+    a = rng.uniform(0.0, 1.0, geo.nb)
+    a[137] = -40.0
+    t, y, x = np.meshgrid(np.arange(T), np.arange(H), np.arange(W), indexing="ij")
+    blk = ((t // tile[0]) * geo.nby + y // tile[1]) * geo.nbx + x // tile[2]
+    blk = blk.reshape(-1)
+    q = 2.0 * u[None, :] + 0.01 * rng.standard_normal((blk.size, 128))
+    k = a[blk][:, None] * u[None, :] + 0.5 * rng.standard_normal((blk.size, 128))
+    Qb = synth.f32_to_bf16_bits(q.astype(np.float32)).reshape(1, 1, -1, 128)
+    Kb = synth.f32_to_bf16_bits(k.astype(np.float32)).reshape(1, 1, -1, 128)
+    mask, counts, _ = check_route("multilevel", Qb, Kb, cfg, 0.9, 4)
+    assert mask[0, 0, :, 137].sum() == 0  # the outlier is never kept
+    assert 0.5 * geo.nb < counts.mean() < geo.nb  # the cut falls inside the cluster
