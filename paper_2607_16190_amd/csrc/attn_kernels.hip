@@ -349,14 +349,12 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         if (nj < 64 * hb + 64) {
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            if (t < 4) {
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const int kap = 64 * hb + 32 * (t >> 1) + 8 * g4 + 4 * (t & 1) + r;
-                if (kap >= nj) {
-                  s[t][0][r] = -INFINITY;
-                  s[t][1][r] = -INFINITY;
-                }
+            for (int r = 0; r < 4; ++r) {
+              const int kap = 64 * hb + 32 * (t >> 1) + 8 * g4 + 4 * (t & 1) + r;
+              if (kap >= nj) {
+                s[t][0][r] = -INFINITY;
+                s[t][1][r] = -INFINITY;
               }
             }
           }
@@ -364,54 +362,51 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
         float mx[2] = {-INFINITY, -INFINITY};
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          if (t < 4) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              mx[0] = fmaxf(mx[0], s[t][0][r]);
-              mx[1] = fmaxf(mx[1], s[t][1][r]);
-            }
+          for (int r = 0; r < 4; ++r) {
+            mx[0] = fmaxf(mx[0], s[t][0][r]);
+            mx[1] = fmaxf(mx[1], s[t][1][r]);
           }
         }
         // The exponent reference mrow only moves when a row's max exceeds it
         // by more than 2^8 (in exp2 units): P stays <= 256, exact in bf16
         // scaling, and the O rescale is rare. O and l share the reference, so
-        // the final O / l is unchanged.
-        float alpha[2], negm[2];
-        bool grow[2];
+        // the final O / l is unchanged. A row's max is the max over its four
+        // lane groups, all in this wave: when no lane's own max passes the
+        // threshold, no row's does, and the cross-lane max is skipped.
+        const bool want0 = (mx[0] - mrow[0]) * P.c2 > 8.0f;
+        const bool want1 = (mx[1] - mrow[1]) * P.c2 > 8.0f;
+        if (__ballot(want0 || want1)) {
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          mx[nt] = row_max4(mx[nt]);
-          grow[nt] = (mx[nt] - mrow[nt]) * P.c2 > 8.0f;
-          const float mref = grow[nt] ? mx[nt] : mrow[nt];
-          alpha[nt] = grow[nt] ? __builtin_amdgcn_exp2f((mrow[nt] - mref) * P.c2) : 1.0f;
-          negm[nt] = -mref * P.c2;
-          mrow[nt] = mref;
+          for (int nt = 0; nt < 2; ++nt) {
+            const float rmx = row_max4(mx[nt]);
+            const bool grow = (rmx - mrow[nt]) * P.c2 > 8.0f;
+            const float mref = grow ? rmx : mrow[nt];
+            const float alpha = grow ? __builtin_amdgcn_exp2f((mrow[nt] - mref) * P.c2) : 1.0f;
+            mrow[nt] = mref;
+            if (__ballot(grow)) {
+#pragma unroll
+              for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha;
+              lsum[nt] *= alpha;
+            }
+          }
         }
+        const float negm[2] = {-mrow[0] * P.c2, -mrow[1] * P.c2};
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-          if (kk < 2) {
 #pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
-              const int t = 2 * kk + hh;
+          for (int hh = 0; hh < 2; ++hh) {
+            const int t = 2 * kk + hh;
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
+            for (int r = 0; r < 4; ++r) {
 #pragma unroll
-                for (int nt = 0; nt < 2; ++nt) {
-                  s[t][nt][r] = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
-                }
+              for (int nt = 0; nt < 2; ++nt) {
+                s[t][nt][r] = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
               }
             }
-            pb[kk][0] = to_bf16x8(s[2 * kk][0], s[2 * kk + 1][0]);
-            pb[kk][1] = to_bf16x8(s[2 * kk][1], s[2 * kk + 1][1]);
           }
-        }
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          if (__ballot(grow[nt])) {
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha[nt];
-            lsum[nt] *= alpha[nt];
-          }
+          pb[kk][0] = to_bf16x8(s[2 * kk][0], s[2 * kk + 1][0]);
+          pb[kk][1] = to_bf16x8(s[2 * kk][1], s[2 * kk + 1][1]);
         }
       }
 
