@@ -24,6 +24,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "fva_common.h"
 #include "fva_geometry.h"
 #include "fva_internal.h"
@@ -175,10 +177,19 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 a, f32x4 b) {
   return __builtin_convertvector(v, bf16x8);
 }
 
-// Key groups (of 32) a block is processed with: blocks of at most 64 keys
-// take one 64-key half, all others both halves (keys past n are masked).
-// With only these two shapes every half runs with constant loop bounds.
-__device__ __forceinline__ int ngroups_of(int n) { return n <= 64 ? 2 : 4; }
+// Calls f(integral_constant<int, u>) for u = B .. E - 1 (compile-time steps).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// Key groups (of 32) a block is processed with: the first 64-key half is
+// always whole, the second holds the remaining groups (none, one or two);
+// keys past n are masked. Each half runs with constant loop bounds.
+__device__ __forceinline__ int ngroups_of(int n) { return n <= 64 ? 2 : (n <= 96 ? 3 : 4); }
 
 // max over lanes l, l^16, l^32, l^48 (the four lane groups holding one
 // query row) with the gfx950 lane-swap instructions; no LDS traffic.
@@ -290,6 +301,132 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
     return *reinterpret_cast<const bf16x8*>(Ks + (mt * 16 + l16) * kRowBytes + 16 * ((4 * ks + g4) ^ l16));
   };
 
+  // One half of a block: S^T for its key groups (LDS tiles 4hb .. 4hb + 3),
+  // the online softmax, and the PV product. A short half (the second half of
+  // a block with 65 .. 96 keys) has only its first group of 32 keys: the
+  // steps of the second group are skipped by uniform branches, so there is
+  // one code path for both shapes. The K (V) fragment of step u + 3 is read
+  // while step u multiplies (a ring of four fragments), so the LDS latency is
+  // covered by six MFMAs.
+  auto s_phase = [&](int hb, bool short_half, f32x4 (&s)[4][2]) {
+    constexpr int kKPre = 3;
+    bf16x8 kq[kKPre + 1];
+#pragma unroll
+    for (int u = 0; u < kKPre; ++u) kq[u] = kfrag(4 * hb + (u >> 2), u & 3);
+    // Issue priority while multiplying: the SIMD's other wave (another
+    // workgroup, usually in its softmax) fills the matrix unit's gaps.
+    __builtin_amdgcn_s_setprio(2);
+    auto step = [&](auto u_c) {
+      constexpr int u = decltype(u_c)::value;
+      constexpr int t = u >> 2, ks = u & 3;
+      if (u + kKPre < 16) kq[(u + kKPre) % (kKPre + 1)] = kfrag(4 * hb + ((u + kKPre) >> 2), (u + kKPre) & 3);
+      const bf16x8 ka = kq[u % (kKPre + 1)];
+      const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+      s[t][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[0][ks], ks == 0 ? z : s[t][0], 0, 0, 0);
+      s[t][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[1][ks], ks == 0 ? z : s[t][1], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    static_for<0, 8>(step);
+    if (!short_half) static_for<8, 16>(step);
+    __builtin_amdgcn_s_setprio(0);
+  };
+
+  // Online softmax over the half. Accumulator (t, r) of lane group g4 holds
+  // key 64hb + 32*(t/2) + 8*g4 + 4*(t%2) + r; keys past nj are masked (in a
+  // short half that covers every key of tiles 2 and 3).
+  auto softmax_phase = [&](int hb, bool short_half, int nj, f32x4 (&s)[4][2], bf16x8 (&pb)[2][2]) {
+    if (nj < 64 * hb + 64) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kap = 64 * hb + 32 * (t >> 1) + 8 * g4 + 4 * (t & 1) + r;
+          if (kap >= nj) {
+            s[t][0][r] = -INFINITY;
+            s[t][1][r] = -INFINITY;
+          }
+        }
+      }
+    }
+    float mx[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        mx[0] = fmaxf(mx[0], s[t][0][r]);
+        mx[1] = fmaxf(mx[1], s[t][1][r]);
+      }
+    }
+    // The exponent reference mrow only moves when a row's max exceeds it
+    // by more than 2^8 (in exp2 units): P stays <= 256, exact in bf16
+    // scaling, and the O rescale is rare. O and l share the reference, so
+    // the final O / l is unchanged. A row's max is the max over its four
+    // lane groups, all in this wave: when no lane's own max passes the
+    // threshold, no row's does, and the cross-lane max is skipped.
+    const bool want0 = (mx[0] - mrow[0]) * P.c2 > 8.0f;
+    const bool want1 = (mx[1] - mrow[1]) * P.c2 > 8.0f;
+    if (__ballot(want0 || want1)) {
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        const float rmx = row_max4(mx[nt]);
+        const bool grow = (rmx - mrow[nt]) * P.c2 > 8.0f;
+        const float mref = grow ? rmx : mrow[nt];
+        const float alpha = grow ? __builtin_amdgcn_exp2f((mrow[nt] - mref) * P.c2) : 1.0f;
+        mrow[nt] = mref;
+        if (__ballot(grow)) {
+#pragma unroll
+          for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha;
+          lsum[nt] *= alpha;
+        }
+      }
+    }
+    const float negm[2] = {-mrow[0] * P.c2, -mrow[1] * P.c2};
+    auto group = [&](auto kk_c) {
+      constexpr int kk = decltype(kk_c)::value;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int t = 2 * kk + hh;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+#pragma unroll
+          for (int nt = 0; nt < 2; ++nt) {
+            s[t][nt][r] = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
+          }
+        }
+      }
+      pb[kk][0] = to_bf16x8(s[2 * kk][0], s[2 * kk + 1][0]);
+      pb[kk][1] = to_bf16x8(s[2 * kk][1], s[2 * kk + 1][1]);
+    };
+    group(std::integral_constant<int, 0>{});
+    if (!short_half) group(std::integral_constant<int, 1>{});
+  };
+
+  // O^T += V^T P^T, 32 keys per MFMA; V^T comes from row-major V through
+  // transposing LDS reads. Step u = 8kk + mt.
+  auto pv_phase = [&](int hb, bool short_half, const bf16x8 (&pb)[2][2]) {
+    constexpr int kVPre = 3;
+    bf16x8 vq[kVPre + 1];
+#pragma unroll
+    for (int u = 0; u < kVPre; ++u) vq[u] = vfrag(2 * hb + (u >> 3), u & 7);
+    __builtin_amdgcn_s_setprio(1);
+    auto step = [&](auto u_c) {
+      constexpr int u = decltype(u_c)::value;
+      constexpr int kk = u >> 3, mt = u & 7;
+      if (u + kVPre < 16) vq[(u + kVPre) % (kVPre + 1)] = vfrag(2 * hb + ((u + kVPre) >> 3), (u + kVPre) & 7);
+      const bf16x8 va = vq[u % (kVPre + 1)];
+      o[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][0], o[mt][0], 0, 0, 0);
+      o[mt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][1], o[mt][1], 0, 0, 0);
+      if (mt == 7) {
+        lsum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][0], lsum[0], 0, 0, 0);
+        lsum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][1], lsum[1], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    static_for<0, 8>(step);
+    if (!short_half) static_for<8, 16>(step);
+    __builtin_amdgcn_s_setprio(0);
+  };
+
   for (int c = 0; c < cnt; ++c) {
     const int nj = mc.n;
     const int ng = ngroups_of(nj);
@@ -298,36 +435,15 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
     tile_barrier();
 
     int ng_next = 0;
-    // Each 128-key block is taken as two halves of 64 keys (key groups 2hb,
-    // 2hb+1): S half -> online softmax -> PV half. Half 1 of a block with at
-    // most 64 real keys is empty.
+    // Each block is taken as two halves of 64 keys (key groups 2hb, 2hb+1):
+    // S half -> online softmax -> PV half. Half 1 holds ng - 2 groups.
 #pragma unroll
     for (int hb = 0; hb < 2; ++hb) {
-      const int ngh = ng > 2 * hb ? 2 : 0;  // key groups in this half (0 or 2)
+      const bool run = hb == 0 || ng > 2;
+      const bool short_half = hb == 1 && ng == 3;
       f32x4 s[4][2];
-      if (active && ngh > 0) {
-        // S^T = K Q^T for LDS tiles 4hb .. 4hb + 3. Step u = 4t + ks; the K
-        // fragment of step u + 3 is read while step u multiplies (a ring of
-        // four fragments), so the LDS latency is covered by six MFMAs.
-        constexpr int kKPre = 3;
-        bf16x8 kq[kKPre + 1];
-#pragma unroll
-        for (int u = 0; u < kKPre; ++u) kq[u] = kfrag(4 * hb + (u >> 2), u & 3);
-        // Issue priority while multiplying: the SIMD's other wave (another
-        // workgroup, usually in its softmax) fills the matrix unit's gaps.
-        __builtin_amdgcn_s_setprio(2);
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int t = u >> 2, ks = u & 3;
-          if (u + kKPre < 16) kq[(u + kKPre) % (kKPre + 1)] = kfrag(4 * hb + ((u + kKPre) >> 2), (u + kKPre) & 3);
-          const bf16x8 ka = kq[u % (kKPre + 1)];
-          const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
-          s[t][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[0][ks], ks == 0 ? z : s[t][0], 0, 0, 0);
-          s[t][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[1][ks], ks == 0 ? z : s[t][1], 0, 0, 0);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        __builtin_amdgcn_s_setprio(0);
-      }
+      bf16x8 pb[2][2];
+      if (active && run) s_phase(hb, short_half, s);
       if (hb == 1) {
         tile_barrier();  // every wave is done with K_c
         // Next block's K streams in while this block finishes.
@@ -341,106 +457,13 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
           }
         }
       }
-
-      bf16x8 pb[2][2];
-      if (active && ngh > 0) {
-        // Online softmax over this half. Accumulator (t, r) of lane group g4
-        // holds key 64hb + 32*(t/2) + 8*g4 + 4*(t%2) + r.
-        if (nj < 64 * hb + 64) {
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int kap = 64 * hb + 32 * (t >> 1) + 8 * g4 + 4 * (t & 1) + r;
-              if (kap >= nj) {
-                s[t][0][r] = -INFINITY;
-                s[t][1][r] = -INFINITY;
-              }
-            }
-          }
-        }
-        float mx[2] = {-INFINITY, -INFINITY};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            mx[0] = fmaxf(mx[0], s[t][0][r]);
-            mx[1] = fmaxf(mx[1], s[t][1][r]);
-          }
-        }
-        // The exponent reference mrow only moves when a row's max exceeds it
-        // by more than 2^8 (in exp2 units): P stays <= 256, exact in bf16
-        // scaling, and the O rescale is rare. O and l share the reference, so
-        // the final O / l is unchanged. A row's max is the max over its four
-        // lane groups, all in this wave: when no lane's own max passes the
-        // threshold, no row's does, and the cross-lane max is skipped.
-        const bool want0 = (mx[0] - mrow[0]) * P.c2 > 8.0f;
-        const bool want1 = (mx[1] - mrow[1]) * P.c2 > 8.0f;
-        if (__ballot(want0 || want1)) {
-#pragma unroll
-          for (int nt = 0; nt < 2; ++nt) {
-            const float rmx = row_max4(mx[nt]);
-            const bool grow = (rmx - mrow[nt]) * P.c2 > 8.0f;
-            const float mref = grow ? rmx : mrow[nt];
-            const float alpha = grow ? __builtin_amdgcn_exp2f((mrow[nt] - mref) * P.c2) : 1.0f;
-            mrow[nt] = mref;
-            if (__ballot(grow)) {
-#pragma unroll
-              for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha;
-              lsum[nt] *= alpha;
-            }
-          }
-        }
-        const float negm[2] = {-mrow[0] * P.c2, -mrow[1] * P.c2};
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const int t = 2 * kk + hh;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-#pragma unroll
-              for (int nt = 0; nt < 2; ++nt) {
-                s[t][nt][r] = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
-              }
-            }
-          }
-          pb[kk][0] = to_bf16x8(s[2 * kk][0], s[2 * kk + 1][0]);
-          pb[kk][1] = to_bf16x8(s[2 * kk][1], s[2 * kk + 1][1]);
-        }
-      }
-
+      if (active && run) softmax_phase(hb, short_half, nj, s, pb);
       if (hb == 0) {
         // V_c landed: nothing was issued after it yet.
         wait_vmem<0>();
         tile_barrier();
       }
-
-      if (active && ngh > 0) {
-        // O^T += V^T P^T, 32 keys per MFMA; V^T comes from row-major V through
-        // transposing LDS reads. Step u = 8kk + mt; the fragment of step u + 3
-        // is read while step u multiplies (a ring of four fragments), so the
-        // LDS latency is covered by six MFMAs.
-        constexpr int kVPre = 3;
-        bf16x8 vq[kVPre + 1];
-#pragma unroll
-        for (int u = 0; u < kVPre; ++u) vq[u] = vfrag(2 * hb + (u >> 3), u & 7);
-        __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int kk = u >> 3, mt = u & 7;
-          if (u + kVPre < 16) vq[(u + kVPre) % (kVPre + 1)] = vfrag(2 * hb + ((u + kVPre) >> 3), (u + kVPre) & 7);
-          const bf16x8 va = vq[u % (kVPre + 1)];
-          o[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][0], o[mt][0], 0, 0, 0);
-          o[mt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[kk][1], o[mt][1], 0, 0, 0);
-          if (mt == 7) {
-            lsum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][0], lsum[0], 0, 0, 0);
-            lsum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][1], lsum[1], 0, 0, 0);
-          }
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        __builtin_amdgcn_s_setprio(0);
-      }
+      if (active && run) pv_phase(hb, short_half, pb);
     }
     tile_barrier();  // every wave is done with V_c
     if (c + 1 < cnt && wave < ng_next) issue_tile<true>(Vh, roff, Vs);
