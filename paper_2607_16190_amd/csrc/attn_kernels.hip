@@ -45,6 +45,8 @@ constexpr int kAttnThreads = 256;
 constexpr int kRowBytes = 256;                 // one 128-dim bf16 row
 constexpr int kTileBytes = 128 * kRowBytes;    // 32 KB per K or V tile
 
+struct BlockMap;
+
 struct AttnParams {
   const uint16_t* Q;
   const uint16_t* K;
@@ -55,6 +57,7 @@ struct AttnParams {
   Geometry g;
   const int32_t* counts;
   const int32_t* kv_idx;
+  const BlockMap* bmap;  // [nb] block records
   float c2;  // softmax scale * log2(e)
   int64_t* trace;
 };
@@ -68,13 +71,17 @@ __device__ __forceinline__ int key_of_row(int rho) {
   return ((rho >> 5) << 5) | (((rho >> 2) & 3) << 3) | (((rho >> 4) & 1) << 2) | (rho & 3);
 }
 
-// Uniform per-block constants for mapping a packed row index to its token.
+// Uniform per-block constants for mapping a packed row index to its token,
+// one 32-byte record per block in the attention workspace (block_table_kernel
+// fills it once per launch, so the block loop does no integer division).
 struct BlockMap {
   int tbase;      // token of the box origin
   int plane, ex;  // ey*ex and ex
   int mp, mx;     // ceil(2^16 / plane), ceil(2^16 / ex): exact quotients for rows < 128
   int n;          // real tokens
+  int pad0, pad1;
 };
+static_assert(sizeof(BlockMap) == 32, "one scalar load per record");
 
 __device__ __forceinline__ BlockMap block_map(const Geometry& g, int j) {
   const BlockBox b = block_box(g, j);
@@ -85,6 +92,24 @@ __device__ __forceinline__ BlockMap block_map(const Geometry& g, int j) {
   m.mp = (65536 + m.plane - 1) / m.plane;
   m.mx = (65536 + m.ex - 1) / m.ex;
   m.n = b.n;
+  m.pad0 = 0;
+  m.pad1 = 0;
+  return m;
+}
+
+// Record of block j through the scalar cache (the kernels never write it).
+__device__ __forceinline__ BlockMap load_block_map(const BlockMap* table, int j) {
+  typedef __attribute__((address_space(4))) const int32_t const_i32;
+  const const_i32* t = (const const_i32*)(table + j);
+  BlockMap m;
+  m.tbase = t[0];
+  m.plane = t[1];
+  m.ex = t[2];
+  m.mp = t[3];
+  m.mx = t[4];
+  m.n = t[5];
+  m.pad0 = 0;
+  m.pad1 = 0;
   return m;
 }
 
@@ -280,9 +305,13 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
   const int vrow = (4 * g4 + te) * kRowBytes;
   const int vsw = (4 * g4 + te) & 7;
 
+  // The kept-block id and block record of the next block are fetched one
+  // block ahead (during the current block's softmax), so their scalar loads
+  // never stall the copy of the next tiles.
   int roff[8];
-  int jc = cnt > 0 ? min(max(kvl[0], 0), nb - 1) : 0;
-  BlockMap mc = block_map(P.g, jc);
+  const int jc = cnt > 0 ? min(max(kvl[0], 0), nb - 1) : 0;
+  BlockMap mc = load_block_map(P.bmap, jc);
+  int j1 = cnt > 1 ? min(max(kvl[1], 0), nb - 1) : 0;
   if (cnt > 0) {
     row_offsets(P, mc, roff);
     if (wave < ngroups_of(mc.n)) {
@@ -435,6 +464,8 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
     tile_barrier();
 
     int ng_next = 0;
+    BlockMap mn;
+    int j2 = 0;
     // Each block is taken as two halves of 64 keys (key groups 2hb, 2hb+1):
     // S half -> online softmax -> PV half. Half 1 holds ng - 2 groups.
 #pragma unroll
@@ -444,12 +475,16 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
       f32x4 s[4][2];
       bf16x8 pb[2][2];
       if (active && run) s_phase(hb, short_half, s);
+      if (hb == 0) {
+        // record of block c + 1 and the id of block c + 2 (clamped to the list)
+        mn = load_block_map(P.bmap, j1);
+        j2 = min(max(kvl[min(c + 2, cnt - 1)], 0), nb - 1);
+      }
       if (hb == 1) {
         tile_barrier();  // every wave is done with K_c
         // Next block's K streams in while this block finishes.
         if (c + 1 < cnt) {
-          const int jn = min(max(kvl[c + 1], 0), nb - 1);
-          mc = block_map(P.g, jn);
+          mc = mn;
           ng_next = ngroups_of(mc.n);
           if (wave < ng_next) {
             row_offsets(P, mc, roff);
@@ -459,6 +494,9 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
       }
       if (active && run) softmax_phase(hb, short_half, nj, s, pb);
       if (hb == 0) {
+        // The prefetched scalars have landed long ago; waiting for them here,
+        // where no LDS read is in flight, keeps the PV fragment waits exact.
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
         // V_c landed: nothing was issued after it yet.
         wait_vmem<0>();
         tile_barrier();
@@ -467,6 +505,7 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
     }
     tile_barrier();  // every wave is done with V_c
     if (c + 1 < cnt && wave < ng_next) issue_tile<true>(Vh, roff, Vs);
+    j1 = j2;
   }
 
   // Epilogue: O^T accumulator (mt, r) of lane (g4, l16) is head dim
@@ -663,6 +702,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   if (threadIdx.x < kQueues) qctr[threadIdx.x] = 0;
 }
 
+// Block records of every block of the tiling (one thread per block).
+__global__ __launch_bounds__(256) void block_table_kernel(Geometry g, BlockMap* __restrict__ table) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j < g.nb) table[j] = block_map(g, j);
+}
+
 // counts and ascending kept-block lists from a block mask, one wave per row.
 __global__ __launch_bounds__(256) void compact_kernel(const uint8_t* __restrict__ mask, int n_rows, int nb,
                                                      int32_t* __restrict__ counts, int32_t* __restrict__ kv_idx) {
@@ -717,6 +762,7 @@ struct AttnWorkspace {
   int32_t* qbase;    // [kQueues + 1]
   int32_t* qctr;     // [kQueues]
   int32_t* hscratch; // [heads * (2 + 2 * kQueues + 1)]
+  BlockMap* bmap;     // [nb]
   size_t bytes;
 };
 
@@ -739,6 +785,8 @@ AttnWorkspace carve(void* base, int batch, int heads, int nb) {
   off += al(kQueues * 4);
   w.hscratch = reinterpret_cast<int32_t*>(p + off);
   off += al(nh * (2 + 2 * kQueues + 1) * 4);
+  w.bmap = reinterpret_cast<BlockMap*>(p + off);
+  off += al((size_t)nb * sizeof(BlockMap));
   w.bytes = off;
   return w;
 }
@@ -781,8 +829,13 @@ hipError_t launch_attn(const AttnArgs& a) {
   P.g = g;
   P.counts = counts;
   P.kv_idx = kv_idx;
+  P.bmap = ws.bmap;
   P.c2 = a.scale * 1.4426950408889634f;
   P.trace = (a.flags & 2u) ? a.trace : nullptr;
+
+  hipLaunchKernelGGL(block_table_kernel, dim3((g.nb + 255) / 256), dim3(256), 0, a.stream, g, ws.bmap);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
 
   if (a.flags & 1u) {
     hipLaunchKernelGGL(attn_naive_kernel, dim3(n_items), dim3(kAttnThreads), 0, a.stream, P);

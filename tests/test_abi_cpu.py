@@ -57,9 +57,10 @@ def test_workspace_sizes():
     # then the fp64 score rows
     assert fva.fva_route_workspace_size(desc(), T720) == 2 * 40 * 672 * 128 * 8 + 40 * nb * nb * 8
     al = lambda x: (x + 255) // 256 * 256
-    # counts, kept lists, queue items, 9 queue bases, 8 queue counters, per-head plan scratch
+    # counts, kept lists, queue items, 9 queue bases, 8 queue counters, per-head plan scratch,
+    # one 32-byte record per block
     heads = 40
-    expect = al(rows * 4) + al(rows * nb * 4) + al(rows * 4) + al(9 * 4) + al(8 * 4) + al(heads * 19 * 4)
+    expect = al(rows * 4) + al(rows * nb * 4) + al(rows * 4) + al(9 * 4) + al(8 * 4) + al(heads * 19 * 4) + al(nb * 32)
     assert fva.fva_attn_workspace_size(desc(), T720) == expect
     assert fva.fva_trace_words(desc(), T720) == rows * 4
 
