@@ -164,13 +164,18 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
   }
 }
 
-// Unnormalised probability exp(s - smax) of a block (s <= smax), evaluated
-// with the hardware exp2 in fp32: relative error below 2^-21, far inside
-// what the Top-p decision needs (the scores themselves, which decide the
-// order, stay fp64). Masses below 2^-126 flush to zero; they are below the
-// 2^-52 quantum of the fixed-point sums anyway.
+// The score rows hold the raw products q_i . k_j; the 1/sqrt(128) score
+// scale enters only here (the order of a row does not depend on it), folded
+// with log2(e) into one factor.
+constexpr double kLog2eOverSqrtD = 0.12751743082459868;  // log2(e) / sqrt(128)
+
+// Unnormalised probability exp((s - smax) / sqrt(128)) of a block (s <= smax,
+// raw products), evaluated with the hardware exp2 in fp32: relative error
+// below 2^-21, far inside what the Top-p decision needs (the scores
+// themselves, which decide the order, stay fp64). Masses below 2^-126 flush
+// to zero; they are below the 2^-52 quantum of the fixed-point sums anyway.
 __device__ __forceinline__ double block_exp(double s, double smax) {
-  return (double)__builtin_amdgcn_exp2f((float)((s - smax) * 1.4426950408889634));
+  return (double)__builtin_amdgcn_exp2f((float)((s - smax) * kLog2eOverSqrtD));
 }
 
 // Nearest integer (ties to even) of x in [0, 2^52]: x + 2^52 rounds to an
@@ -458,12 +463,12 @@ __device__ __forceinline__ int xcd_contiguous(int n, int total) {
   return x * q + min(x, r) + (n >> 3);
 }
 
-// Scores s_ij = qbar_i . kbar_j / sqrt(128) of 16 query blocks against every
-// key block with the fp64 MFMA (16x16x4): lane (row l%16, group g = l/16)
-// feeds dim 32g + k of its query row and its key at step k, so the 32 steps
-// sum the full 128-dim dot product. Wave w takes key tiles w, w+4, ... The
-// grid is one-dimensional over (head, query tile); scores go to a row-major
-// [B*H*nb, nb] fp64 buffer.
+// Raw products qbar_i . kbar_j (the score s_ij times sqrt(128)) of 16 query
+// blocks against every key block with the fp64 MFMA (16x16x4): lane (row
+// l%16, group g = l/16) feeds dim 32g + k of its query row and its key at
+// step k, so the 32 steps sum the full 128-dim dot product. Wave w takes key
+// tiles w, w+4, ... The grid is one-dimensional over (head, query tile); the
+// products go to a row-major [B*H*nb, nb] fp64 buffer.
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __restrict__ qbar,
                                                              const double* __restrict__ kbar, int nb,
                                                              double* __restrict__ scores) {
@@ -477,7 +482,6 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __re
   const int nwaves = kScoreThreads / 64;
   const int m16 = lane & 15;
   const int g = lane >> 4;
-  const double inv_sqrt_d = 11.313708498984761;  // sqrt(128): s = dot / sqrt(128)
 
   // Operands in the order written by pool_kernel: MFMA step k = 2u + e of
   // lane (m16, g) multiplies dim 32g + 2u + e of query row m16 and key m16 of
@@ -518,7 +522,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __re
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int r = g + 4 * e;
-        if (i0 + r < nb) srow[(int64_t)r * nb + key] = __ddiv_rn(acc[e], inv_sqrt_d);
+        if (i0 + r < nb) srow[(int64_t)r * nb + key] = acc[e];
       }
     }
   };
