@@ -72,6 +72,12 @@ typedef struct fva_qkv_desc {
 #define FVA_SCHED_PERSISTENT 0u /* persistent grid pulling (head, query-block) items, heaviest first */
 #define FVA_SCHED_NAIVE 1u      /* one workgroup per item in head-major order (same kernel body) */
 #define FVA_TRACE 2u            /* record per-item start/end clock and CU id into `trace` */
+/* Persistent scheduler only: split every row keeping more than s blocks into
+ * ceil(count / s) chunk items of at most s blocks (1 <= s <= 65535). Without
+ * it the chunk size is automatic: max(32, ceil(total / 1024)) with total the
+ * sum over rows of (kept blocks + 1), so rows are split only when there are
+ * few of them per workgroup slot. */
+#define FVA_SPLIT_BLOCKS(s) (((uint32_t)(s) & 0xFFFFu) << 8)
 
 /* Number of blocks of a tiling, or -1 if an extent is not positive. Host only. */
 int32_t fva_num_blocks(const fva_tiling* tiling);
@@ -114,13 +120,18 @@ fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, dou
 
 /*
  * Workspace bytes needed by fva_attn for this shape and flags: the work
- * list and queue counters, plus room for counts and kv_idx (batch*heads*nb
- * and batch*heads*nb*nb int32) used when the caller passes them as NULL.
+ * list and queue counters, room for counts and kv_idx (batch*heads*nb and
+ * batch*heads*nb*nb int32) used when the caller passes them as NULL, one
+ * 32-byte record per block, and the partial results of split rows: 66,560
+ * bytes per chunk for at most 2048 chunks (automatic chunk size) or
+ * batch*heads*nb*ceil(nb/s) chunks under FVA_SPLIT_BLOCKS(s); none under
+ * FVA_SCHED_NAIVE.
  */
 fva_status fva_attn_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, uint32_t flags,
                                    size_t* bytes);
 
-/* Number of int64 words `trace` must hold under FVA_TRACE: 4 per (b, h, i) row. */
+/* Number of int64 words `trace` must hold under FVA_TRACE: 4 per (b, h, i)
+ * row, then 4 for each of up to 2048 chunk items of split rows. */
 int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling);
 
 /*
@@ -138,12 +149,16 @@ int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling);
  *          workspace) or both given in the layout fva_route writes, and then
  *          they must describe block_mask exactly.
  * softmax_scale: <= 0 selects 1/sqrt(128).
- * flags: FVA_SCHED_PERSISTENT or FVA_SCHED_NAIVE, optionally | FVA_TRACE.
+ * flags: FVA_SCHED_PERSISTENT or FVA_SCHED_NAIVE, optionally | FVA_TRACE
+ *        and | FVA_SPLIT_BLOCKS(s). A split row's chunks run as separate
+ *        work items; their partial results (fp32) are merged in chunk order,
+ *        so results stay deterministic.
  * O: bf16, same strides as Q; every real token row is written.
  * trace: device int64 [fva_trace_words] when FVA_TRACE is set, else ignored.
  *        Row r = (b*heads + h)*nb + i gets {start clock, end clock,
- *        (xcc_id << 16) | hw_id low bits, workgroup id}; clocks are the
- *        100 MHz constant device clock.
+ *        (xcc_id << 16) | hw_id low bits, workgroup id} (unwritten for a
+ *        split row), chunk c of a split row the same at batch*heads*nb + c
+ *        (c < 2048); clocks are the 100 MHz constant device clock.
  */
 fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_desc* desc,
                     const fva_tiling* tiling, const uint8_t* block_mask, const int32_t* counts,

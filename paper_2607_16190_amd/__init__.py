@@ -29,6 +29,11 @@ FVA_SCHED_PERSISTENT = 0
 FVA_SCHED_NAIVE = 1
 FVA_TRACE = 2
 
+
+def FVA_SPLIT_BLOCKS(s: int) -> int:
+    """Flag bits forcing chunks of at most s kept blocks per split row (persistent scheduler)."""
+    return (int(s) & 0xFFFF) << 8
+
 EXPORTED = (
     "fva_num_blocks",
     "fva_route_workspace_size",
@@ -222,7 +227,7 @@ def fva_attn(q, k, v, tiling: Tiling, mask, counts=None, kv_idx=None, *, scale: 
         out = torch.empty_strided(q.shape, q.stride(), dtype=torch.bfloat16, device=q.device)
     elif out.stride() != q.stride() or out.shape != q.shape or out.dtype != torch.bfloat16:
         raise ValueError("out must match q in shape, strides and dtype")
-    ws = _workspace(torch, fva_attn_workspace_size(desc, tiling, flags & 3), q.device, workspace)
+    ws = _workspace(torch, fva_attn_workspace_size(desc, tiling, flags), q.device, workspace)
     if (flags & FVA_TRACE) and trace is None:
         raise ValueError("FVA_TRACE needs a trace tensor of fva_trace_words int64")
     st = lib.fva_attn(

@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "fva_common.h"
@@ -44,6 +45,10 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 constexpr int kAttnThreads = 256;
 constexpr int kRowBytes = 256;                 // one 128-dim bf16 row
 constexpr int kTileBytes = 128 * kRowBytes;    // 32 KB per K or V tile
+// Partial result of one chunk of a split row: O^T accumulators as
+// [128 query rows][128 dims] fp32, then the exponent reference and the sum of
+// P of every query row (fp32 [128] each).
+constexpr int kPartialFloats = 128 * 128 + 2 * 128;
 
 struct BlockMap;
 
@@ -58,6 +63,10 @@ struct AttnParams {
   const int32_t* counts;
   const int32_t* kv_idx;
   const BlockMap* bmap;  // [nb] block records
+  const int4* chunks;    // [chunks] (row, first kept entry, end, 0) of split rows
+  float* partials;       // [chunks][kPartialFloats] unnormalised O, reference, sum
+  int64_t n_rows;        // batch * heads * nb
+  int trace_chunks;      // chunk records the trace holds after the rows
   float c2;  // softmax scale * log2(e)
   int64_t* trace;
 };
@@ -235,11 +244,15 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // S^T tiles of one 64-key half: LDS tiles 4hb .. 4hb + 2*NGH - 1 against the
 // two 16-row Q tiles. The fragments of tile t+1 load while tile t multiplies
 // (two fragment buffers, renamed at compile time).
-__device__ void process_item(const AttnParams& P, int item, unsigned char* __restrict__ Ks,
-                             unsigned char* __restrict__ Vs) {
+// One work item: query block `row` (= (b * heads + h) * nb + i) against the
+// kept-list entries [begin, end) of its row. partial == nullptr: the whole
+// row, normalised into O; otherwise one chunk of a split row, whose
+// unnormalised result goes to partial for the combine step.
+__device__ void process_item(const AttnParams& P, int row, int begin, int end, float* __restrict__ partial,
+                             unsigned char* __restrict__ Ks, unsigned char* __restrict__ Vs) {
   const int nb = P.g.nb;
-  const int bh = item / nb;
-  const int i = item - bh * nb;
+  const int bh = row / nb;
+  const int i = row - bh * nb;
   const int b = bh / P.heads;
   const int h = bh - b * P.heads;
   const int64_t base = (int64_t)b * P.sb + (int64_t)h * P.sh;
@@ -259,8 +272,11 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
   // space: the kernel never writes them). They come from the caller: clamp
   // so a bad list cannot address outside the tensors.
   typedef __attribute__((address_space(4))) const int32_t const_i32;
-  const const_i32* kvl = (const const_i32*)(P.kv_idx + (int64_t)item * nb);
-  const int cnt = min(max(((const const_i32*)P.counts)[item], 0), nb);
+  const int full = min(max(((const const_i32*)P.counts)[row], 0), nb);
+  begin = min(max(begin, 0), full);
+  end = min(max(end, begin), full);
+  const const_i32* kvl = (const const_i32*)(P.kv_idx + (int64_t)row * nb + begin);
+  const int cnt = end - begin;
 
   // Q_i^T as the B operand: lane holds query row l16 of each 16-row tile,
   // head dims 32ks + 8g4 .. +7.
@@ -510,6 +526,23 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
 
   // Epilogue: O^T accumulator (mt, r) of lane (g4, l16) is head dim
   // 16mt + 4g4 + r of query row 16nt + l16.
+  if (active && partial) {
+    // chunk of a split row: O^T as is, the reference and the sum of P
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      const int r = row0 + 16 * nt + l16;
+      if (r < bi.n) {
+        float* prow = partial + r * 128 + 4 * g4;
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) *reinterpret_cast<f32x4*>(prow + 16 * mt) = o[mt][nt];
+        if (g4 == 0) {
+          partial[128 * 128 + r] = mrow[nt];
+          partial[128 * 128 + 128 + r] = lsum[nt][0];
+        }
+      }
+    }
+    return;
+  }
   if (active) {
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
@@ -526,10 +559,11 @@ __device__ void process_item(const AttnParams& P, int item, unsigned char* __res
   }
 }
 
-__device__ __forceinline__ void trace_item(const AttnParams& P, int item, int64_t t0) {
+// Trace record r: rows first, then chunk items (chunk c at n_rows + c).
+__device__ __forceinline__ void trace_item(const AttnParams& P, int64_t rec, int64_t t0) {
   if (P.trace && threadIdx.x == 0) {
     const int64_t t1 = (int64_t)wall_clock64();
-    int64_t* tr = P.trace + (int64_t)item * 4;
+    int64_t* tr = P.trace + rec * 4;
     tr[0] = t0;
     tr[1] = t1;
     tr[2] = (int64_t)hw_location();
@@ -541,7 +575,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams 
   __shared__ __align__(16) unsigned char ks_tile[kTileBytes];
   __shared__ __align__(16) unsigned char vs_tile[kTileBytes];
   const int64_t t0 = (int64_t)wall_clock64();
-  process_item(P, blockIdx.x, ks_tile, vs_tile);
+  process_item(P, blockIdx.x, 0, P.g.nb, nullptr, ks_tile, vs_tile);
   if (P.trace) {
     __syncthreads();
     trace_item(P, blockIdx.x, t0);
@@ -586,45 +620,156 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
     const int slot = __builtin_amdgcn_readfirstlane(next_slot);
     q = __builtin_amdgcn_readfirstlane(next_q);  // keep stealing from a queue that had work
     if (slot < 0) break;
+    // item >= 0: a whole row; item < 0: chunk -1 - item of a split row
     const int item = __builtin_amdgcn_readfirstlane(items[slot]);
     const int64_t t0 = (int64_t)wall_clock64();
-    process_item(P, item, ks_tile, vs_tile);
+    int64_t rec;
+    if (item >= 0) {
+      process_item(P, item, 0, P.g.nb, nullptr, ks_tile, vs_tile);
+      rec = item;
+    } else {
+      const int c = -1 - item;
+      typedef __attribute__((address_space(4))) const int32_t const_i32;
+      const const_i32* ch = (const const_i32*)(P.chunks + c);
+      process_item(P, ch[0], ch[1], ch[2], P.partials + (int64_t)c * kPartialFloats, ks_tile, vs_tile);
+      rec = c < P.trace_chunks ? P.n_rows + c : -1;
+    }
     __syncthreads();  // the next item's copies overwrite the tiles; next_slot is rewritten
-    if (P.trace) trace_item(P, item, t0);
+    if (P.trace && rec >= 0) trace_item(P, rec, t0);
   }
 }
 
-// Builds the per-XCD queues (one workgroup). Heads are taken in decreasing
-// order of cost (sum over rows of kept blocks + 1). Each head's query blocks
-// are cut into kQueues contiguous runs of about equal cost, run x going to
-// queue x, so all XCDs work on the same head at the same time (its K/V stay
-// in the shared last-level cache) and the resident workgroups of one XCD
-// work on neighbouring query blocks (their kept K/V blocks overlap in L2).
-// Scratch per head: cost, rank, run starts [kQueues + 1], queue offsets [kQueues].
+// Exclusive prefix over the 1024 threads of a workgroup of one int per
+// thread; *total gets the sum. wsum: LDS scratch of 16 ints.
+__device__ __forceinline__ int block_excl_scan(int v, int* wsum, int* total) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int incl = wave_incl_scan_i32(v, lane);
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int before = 0, all = 0;
+  for (int w = 0; w < 16; ++w) {
+    const int t = wsum[w];
+    before += w < wave ? t : 0;
+    all += t;
+  }
+  __syncthreads();
+  *total = all;
+  return before + incl - v;
+}
+
+constexpr int kMinChunk = 32;  // smallest automatic chunk (kept blocks)
+
+// Builds the work list (one workgroup of 1024 threads).
+//
+// Chunks (the split part of the scheduler): with S = `forced` (> 0) or, by
+// default, S = max(kMinChunk, ceil(total / (2 * slots))), total being the sum
+// over rows of (kept blocks + 1), a row keeping more than S blocks becomes
+// ceil(count / S) chunk items of nearly equal length, each a separate work
+// item whose partial result combine_kernel merges. The default S splits only
+// rows longer than about half a workgroup slot's fair share, so with many
+// rows per slot nothing is split; it also bounds the chunks by 4 * slots
+// (the sum of ceil(c / S) over rows with c > S is at most 2 * total / S). If
+// the chunks would exceed chunk_cap, no row is split.
+//
+// Queues: heads are taken in decreasing order of cost. Each head's query
+// blocks are cut into kQueues contiguous runs of about equal cost, run x going
+// to queue x (the items of a split row stay together), so all XCDs work on the
+// same head at the same time (its K/V stay in the shared last-level cache)
+// and the resident workgroups of one XCD work on neighbouring query blocks
+// (their kept K/V blocks overlap in L2).
+//
+// Scratch: per head cost, rank, run starts [kQueues + 1], queue offsets
+// [kQueues]; per row the exclusive prefixes of items, chunks and split rows.
 __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ counts, int n_heads, Geometry g,
-                                                   int32_t* __restrict__ items, int32_t* __restrict__ qbase,
-                                                   int32_t* __restrict__ qctr, int32_t* __restrict__ hscratch) {
+                                                   int slots, int forced, int chunk_cap, int32_t* __restrict__ items,
+                                                   int32_t* __restrict__ qbase, int32_t* __restrict__ qctr,
+                                                   int32_t* __restrict__ hscratch, int32_t* __restrict__ rscratch,
+                                                   int4* __restrict__ chunks, int4* __restrict__ splits,
+                                                   int32_t* __restrict__ n_split) {
+  __shared__ int wsum[16];
+  __shared__ long long wtot[16];
   const int nb = g.nb;
+  const int rows = n_heads * nb;
   int32_t* hcost = hscratch;
   int32_t* horder = hcost + n_heads;
   int32_t* hstart = horder + n_heads;                  // [n_heads][kQueues + 1]
   int32_t* hoff = hstart + (size_t)n_heads * (kQueues + 1);  // [n_heads][kQueues]
+  int32_t* ipre = rscratch;                            // [rows + 1] items before row r
+  int32_t* cpre = ipre + rows + 1;                     // [rows + 1] chunks before row r
+  int32_t* spre = cpre + rows + 1;                     // [rows + 1] split rows before row r
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
-  auto cost_of = [&](int h, int r) {
-    const int c = counts[(int64_t)h * nb + r];
-    return (c < 0 ? 0 : (c > nb ? nb : c)) + 1;
+  auto kept_of = [&](int r) {
+    const int c = counts[r];
+    return c < 0 ? 0 : (c > nb ? nb : c);
   };
+  auto cost_of = [&](int h, int r) { return kept_of(h * nb + r) + 1; };
 
-  // 1. head costs and equal-cost runs (one wave per head)
-  for (int h = wave; h < n_heads; h += nwaves) {
-    int total = 0;
-    for (int i0 = 0; i0 < nb; i0 += 64) total += (i0 + lane < nb) ? cost_of(h, i0 + lane) : 0;
+  // 0. chunk size
+  long long tsum = 0;
+  for (int r = threadIdx.x; r < rows; r += blockDim.x) tsum += kept_of(r) + 1;
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) total += __shfl_xor(total, o);
-    if (lane == 0) hcost[h] = total;
-    // run of row i = floor(kQueues * (cost before row i) / total), a
+  for (int o = 32; o > 0; o >>= 1) tsum += __shfl_xor(tsum, o);
+  if (lane == 0) wtot[wave] = tsum;
+  __syncthreads();
+  long long total = 0;
+  for (int w = 0; w < nwaves; ++w) total += wtot[w];
+  int S = forced > 0 ? forced : (int)max((long long)kMinChunk, (total + 2LL * slots - 1) / (2LL * slots));
+
+  // 1. items per row (1, or its chunks) and the three exclusive prefixes,
+  //    each thread taking a contiguous run of rows
+  const int seg = (rows + (int)blockDim.x - 1) / (int)blockDim.x;
+  const int r0 = min((int)threadIdx.x * seg, rows);
+  const int r1 = min(r0 + seg, rows);
+  for (int attempt = 0; attempt < 2; ++attempt) {
+    auto nchunks = [&](int r) {
+      const int c = kept_of(r);
+      return c > S ? (c + S - 1) / S : 1;
+    };
+    int li = 0, lc = 0, ls = 0;
+    for (int r = r0; r < r1; ++r) {
+      const int n = nchunks(r);
+      li += n;
+      lc += n > 1 ? n : 0;
+      ls += n > 1 ? 1 : 0;
+    }
+    int ti, tc, ts;
+    int bi = block_excl_scan(li, wsum, &ti);
+    int bc = block_excl_scan(lc, wsum, &tc);
+    int bs = block_excl_scan(ls, wsum, &ts);
+    if (tc > chunk_cap && attempt == 0) {
+      S = 0x7fffffff;  // nothing is split
+      continue;
+    }
+    for (int r = r0; r < r1; ++r) {
+      const int n = nchunks(r);
+      ipre[r] = bi;
+      cpre[r] = bc;
+      spre[r] = bs;
+      bi += n;
+      bc += n > 1 ? n : 0;
+      bs += n > 1 ? 1 : 0;
+    }
+    if (threadIdx.x == 0) {
+      ipre[rows] = ti;
+      cpre[rows] = tc;
+      spre[rows] = ts;
+      *n_split = ts;
+    }
+    break;
+  }
+  __syncthreads();
+
+  // 2. head costs and equal-cost runs (one wave per head)
+  for (int h = wave; h < n_heads; h += nwaves) {
+    int hsum = 0;
+    for (int i0 = 0; i0 < nb; i0 += 64) hsum += (i0 + lane < nb) ? cost_of(h, i0 + lane) : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) hsum += __shfl_xor(hsum, o);
+    if (lane == 0) hcost[h] = hsum;
+    // run of row i = floor(kQueues * (cost before row i) / hsum), a
     // non-decreasing function of i; run x starts at the first row whose run
     // is >= x (nb when there is none).
     int stx[kQueues + 1];
@@ -636,7 +781,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
       const int c = i < nb ? cost_of(h, i) : 0;
       const int incl = wave_incl_scan_i32(c, lane);
       const int before = run_before + incl - c;
-      const int run = (int)(((int64_t)before * kQueues) / total);
+      const int run = (int)(((int64_t)before * kQueues) / hsum);
 #pragma unroll
       for (int x = 0; x < kQueues; ++x) {
         const uint64_t hit = __ballot(i < nb && run >= x);
@@ -652,7 +797,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   }
   __syncthreads();
 
-  // 2. head order by decreasing cost (ties: lower head first)
+  // 3. head order by decreasing cost (ties: lower head first)
   for (int h = threadIdx.x; h < n_heads; h += blockDim.x) {
     const int ch = hcost[h];
     int rank = 0;
@@ -664,7 +809,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   }
   __syncthreads();
 
-  // 3. queue offsets of every (head, run) and queue bases
+  // 4. queue offsets (in items) of every (head, run) and queue bases
   if (threadIdx.x < kQueues) {
     const int x = threadIdx.x;
     int run = 0;
@@ -672,7 +817,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
       const int h = horder[r];
       const int32_t* st = hstart + (size_t)h * (kQueues + 1);
       hoff[(size_t)h * kQueues + x] = run;
-      run += st[x + 1] - st[x];
+      run += ipre[h * nb + st[x + 1]] - ipre[h * nb + st[x]];
     }
     qctr[x] = run;  // queue length for now
   }
@@ -688,18 +833,73 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   }
   __syncthreads();
 
-  // 4. scatter items into their queues, reset the queue counters
-  const int n_items = n_heads * nb;
-  for (int r = threadIdx.x; r < n_items; r += blockDim.x) {
+  // 5. scatter items (a split row's chunks consecutively), chunk and split
+  //    records; reset the queue counters
+  for (int r = threadIdx.x; r < rows; r += blockDim.x) {
     const int h = r / nb;
     const int i = r - h * nb;
     const int32_t* st = hstart + (size_t)h * (kQueues + 1);
     int x = 0;
     while (x + 1 < kQueues && st[x + 1] <= i) ++x;
-    items[qbase[x] + hoff[(size_t)h * kQueues + x] + (i - st[x])] = r;
+    const int pos = qbase[x] + hoff[(size_t)h * kQueues + x] + (ipre[r] - ipre[h * nb + st[x]]);
+    const int n = ipre[r + 1] - ipre[r];
+    if (n == 1) {
+      items[pos] = r;
+    } else {
+      const int c0 = cpre[r];
+      const int cnt = kept_of(r);
+      for (int c = 0; c < n; ++c) {
+        items[pos + c] = -1 - (c0 + c);
+        chunks[c0 + c] = make_int4(r, (int)(((int64_t)c * cnt) / n), (int)(((int64_t)(c + 1) * cnt) / n), 0);
+      }
+      splits[spre[r]] = make_int4(r, c0, n, 0);
+    }
   }
   __syncthreads();
   if (threadIdx.x < kQueues) qctr[threadIdx.x] = 0;
+}
+
+// Merges the chunks of every split row (one workgroup per row at a time, in
+// chunk order, so the result is deterministic): with m_c the chunk's
+// exponent reference, l_c its sum of P and O_c its unnormalised output,
+// O = sum_c w_c O_c / sum_c w_c l_c, w_c = exp2((m_c - max_c m_c) * c2).
+// Thread t takes query row t / 2, head dims 64 (t % 2) .. +63.
+__global__ __launch_bounds__(256) void combine_kernel(AttnParams P, const int4* __restrict__ splits,
+                                                     const int32_t* __restrict__ n_split) {
+  const int ns = __builtin_amdgcn_readfirstlane(*n_split);
+  const int nb = P.g.nb;
+  const int q = threadIdx.x >> 1;
+  const int half = threadIdx.x & 1;
+  for (int si = blockIdx.x; si < ns; si += gridDim.x) {
+    const int4 sp = splits[si];
+    const int row = sp.x, c0 = sp.y, n = sp.z;
+    const int bh = row / nb;
+    const int i = row - bh * nb;
+    const int b = bh / P.heads;
+    const int h = bh - b * P.heads;
+    const BlockBox bi = block_box(P.g, i);
+    if (q >= bi.n) continue;
+    const float* part0 = P.partials + (int64_t)c0 * kPartialFloats;
+    float M = -INFINITY;
+    for (int c = 0; c < n; ++c) M = fmaxf(M, part0[(int64_t)c * kPartialFloats + 128 * 128 + q]);
+    f32x4 acc[16];
+#pragma unroll
+    for (int d = 0; d < 16; ++d) acc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float L = 0.f;
+    for (int c = 0; c < n; ++c) {
+      const float* pc = part0 + (int64_t)c * kPartialFloats;
+      const float w = __builtin_amdgcn_exp2f((pc[128 * 128 + q] - M) * P.c2);
+      L += w * pc[128 * 128 + 128 + q];
+      const f32x4* src = reinterpret_cast<const f32x4*>(pc + q * 128 + 64 * half);
+#pragma unroll
+      for (int d = 0; d < 16; ++d) acc[d] += w * src[d];
+    }
+    const float inv = L > 0.f ? 1.0f / L : 0.f;
+    const int64_t base = (int64_t)b * P.sb + (int64_t)h * P.sh;
+    uint16_t* orow = P.O + base + (int64_t)box_token(P.g, bi, q) * P.sn + 64 * half;
+#pragma unroll
+    for (int d = 0; d < 16; ++d) *reinterpret_cast<bf16x4*>(orow + 4 * d) = __builtin_convertvector(acc[d] * inv, bf16x4);
+  }
 }
 
 // Block records of every block of the tiling (one thread per block).
@@ -758,33 +958,64 @@ namespace {
 struct AttnWorkspace {
   int32_t* counts;   // [rows]        rebuilt counts (caller passed none)
   int32_t* kv;       // [rows][nb]    rebuilt kept lists
-  int32_t* items;    // [rows]        queue contents
+  int32_t* items;    // [rows + cap]  queue contents
   int32_t* qbase;    // [kQueues + 1]
   int32_t* qctr;     // [kQueues]
   int32_t* hscratch; // [heads * (2 + 2 * kQueues + 1)]
-  BlockMap* bmap;     // [nb]
+  int32_t* rscratch; // [3 * (rows + 1)] per-row prefixes
+  int32_t* n_split;  // [1]
+  int4* chunks;      // [cap]
+  int4* splits;      // [cap]
+  float* partials;   // [cap][kPartialFloats]
+  BlockMap* bmap;    // [nb]
+  int cap;           // chunk records
   size_t bytes;
 };
 
-AttnWorkspace carve(void* base, int batch, int heads, int nb) {
+// The automatic chunk size assumes kSplitSlots workgroup slots (two per CU of
+// a 256-CU device), which bounds the chunks by 4 * kSplitSlots whatever the
+// device; a forced size s bounds them by rows * ceil(nb / s).
+constexpr int kSplitSlots = 512;
+
+int chunk_cap(int batch, int heads, int nb, uint32_t flags) {
+  if (flags & 1u) return 0;  // one workgroup per row: nothing is split
+  const int forced = (int)((flags >> 8) & 0xFFFFu);
+  if (forced == 0) return 4 * kSplitSlots;
+  const int64_t cap = (int64_t)batch * heads * nb * ((nb + forced - 1) / forced);
+  return (int)std::min<int64_t>(cap, (int64_t)1 << 28);
+}
+
+AttnWorkspace carve(void* base, int batch, int heads, int nb, uint32_t flags) {
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t rows = (size_t)batch * heads * nb;
   const size_t nh = (size_t)batch * heads;
   char* p = reinterpret_cast<char*>(base);
   AttnWorkspace w;
+  w.cap = chunk_cap(batch, heads, nb, flags);
+  const size_t cap = (size_t)w.cap;
   size_t off = 0;
   w.counts = reinterpret_cast<int32_t*>(p + off);
   off += al(rows * 4);
   w.kv = reinterpret_cast<int32_t*>(p + off);
   off += al(rows * nb * 4);
   w.items = reinterpret_cast<int32_t*>(p + off);
-  off += al(rows * 4);
+  off += al((rows + cap) * 4);
   w.qbase = reinterpret_cast<int32_t*>(p + off);
   off += al((kQueues + 1) * 4);
   w.qctr = reinterpret_cast<int32_t*>(p + off);
   off += al(kQueues * 4);
   w.hscratch = reinterpret_cast<int32_t*>(p + off);
   off += al(nh * (2 + 2 * kQueues + 1) * 4);
+  w.rscratch = reinterpret_cast<int32_t*>(p + off);
+  off += al(3 * (rows + 1) * 4);
+  w.n_split = reinterpret_cast<int32_t*>(p + off);
+  off += al(4);
+  w.chunks = reinterpret_cast<int4*>(p + off);
+  off += al(cap * sizeof(int4));
+  w.splits = reinterpret_cast<int4*>(p + off);
+  off += al(cap * sizeof(int4));
+  w.partials = reinterpret_cast<float*>(p + off);
+  off += al(cap * kPartialFloats * sizeof(float));
   w.bmap = reinterpret_cast<BlockMap*>(p + off);
   off += al((size_t)nb * sizeof(BlockMap));
   w.bytes = off;
@@ -792,14 +1023,20 @@ AttnWorkspace carve(void* base, int batch, int heads, int nb) {
 }
 }  // namespace
 
-size_t attn_workspace_bytes(int batch, int heads, int nb) { return carve(nullptr, batch, heads, nb).bytes; }
+size_t attn_workspace_bytes(int batch, int heads, int nb, uint32_t flags) {
+  return carve(nullptr, batch, heads, nb, flags).bytes;
+}
+
+int64_t attn_trace_words(int batch, int heads, int nb) {
+  return 4 * ((int64_t)batch * heads * nb + 4 * kSplitSlots);
+}
 
 hipError_t launch_attn(const AttnArgs& a) {
   (void)hipGetLastError();  // drop an error left by an unrelated earlier HIP call
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
   const int n_items = a.batch * a.heads * g.nb;
   if (n_items == 0) return hipSuccess;
-  const AttnWorkspace ws = carve(a.workspace, a.batch, a.heads, g.nb);
+  const AttnWorkspace ws = carve(a.workspace, a.batch, a.heads, g.nb, a.flags);
   int32_t* ws_counts = ws.counts;
   int32_t* ws_kv = ws.kv;
   DeviceInfo info;
@@ -830,6 +1067,10 @@ hipError_t launch_attn(const AttnArgs& a) {
   P.counts = counts;
   P.kv_idx = kv_idx;
   P.bmap = ws.bmap;
+  P.chunks = ws.chunks;
+  P.partials = ws.partials;
+  P.n_rows = n_items;
+  P.trace_chunks = 4 * kSplitSlots;
   P.c2 = a.scale * 1.4426950408889634f;
   P.trace = (a.flags & 2u) ? a.trace : nullptr;
 
@@ -841,15 +1082,24 @@ hipError_t launch_attn(const AttnArgs& a) {
     hipLaunchKernelGGL(attn_naive_kernel, dim3(n_items), dim3(kAttnThreads), 0, a.stream, P);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, a.batch * a.heads, g, ws.items,
-                     ws.qbase, ws.qctr, ws.hscratch);
+  const int forced = (int)((a.flags >> 8) & 0xFFFFu);
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, a.batch * a.heads, g, kSplitSlots, forced,
+                     ws.cap, ws.items, ws.qbase, ws.qctr, ws.hscratch, ws.rscratch, ws.chunks, ws.splits, ws.n_split);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   int grid = info.cus * info.per_cu;
-  if (grid > n_items) grid = n_items;
+  if (grid > n_items + ws.cap) grid = n_items + ws.cap;
   hipLaunchKernelGGL(attn_persistent_kernel, dim3(grid), dim3(kAttnThreads), 0, a.stream, P, ws.items, ws.qbase,
                      ws.qctr);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // Split rows (if any) are merged; the workgroups beyond their number exit.
+  if (g.nb > (forced > 0 ? forced : kMinChunk)) {
+    const int cgrid = std::max(1, std::min(ws.cap / 2, 2 * info.cus));
+    hipLaunchKernelGGL(combine_kernel, dim3(cgrid), dim3(256), 0, a.stream, P, ws.splits, ws.n_split);
+    e = hipGetLastError();
+  }
+  return e;
 }
 
 }  // namespace fva

@@ -38,6 +38,9 @@ fva_status check_shape(const fva_qkv_desc* d, const fva_tiling* t, int* nb_out) 
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Scheduling bits, the trace bit and a forced chunk size in bits 8..23.
+constexpr uint32_t kAttnFlags = 3u | (0xFFFFu << 8);
+
 }  // namespace
 
 extern "C" {
@@ -60,18 +63,18 @@ fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* 
 
 fva_status fva_attn_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, uint32_t flags, size_t* bytes) {
   if (!bytes) return FVA_ERR_INVALID_ARG;
-  if (flags & ~3u) return FVA_ERR_INVALID_ARG;
+  if (flags & ~kAttnFlags) return FVA_ERR_INVALID_ARG;
   int nb = 0;
   const fva_status s = check_shape(desc, tiling, &nb);
   if (s != FVA_OK) return s;
-  *bytes = fva::attn_workspace_bytes(desc->batch, desc->heads, nb);
+  *bytes = fva::attn_workspace_bytes(desc->batch, desc->heads, nb, flags);
   return FVA_OK;
 }
 
 int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling) {
   int nb = 0;
   if (check_shape(desc, tiling, &nb) != FVA_OK) return -1;
-  return (int64_t)desc->batch * desc->heads * nb * 4;
+  return fva::attn_trace_words(desc->batch, desc->heads, nb);
 }
 
 fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
@@ -114,7 +117,7 @@ fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_d
                     const uint8_t* block_mask, const int32_t* counts, const int32_t* kv_idx, float softmax_scale,
                     uint32_t flags, void* O, void* workspace, size_t workspace_bytes, void* trace, void* stream) {
   if (!Q || !K || !V || !O) return FVA_ERR_INVALID_ARG;
-  if (flags & ~3u) return FVA_ERR_INVALID_ARG;
+  if (flags & ~kAttnFlags) return FVA_ERR_INVALID_ARG;
   if ((counts == nullptr) != (kv_idx == nullptr)) return FVA_ERR_INVALID_ARG;
   if (!counts && !block_mask) return FVA_ERR_INVALID_ARG;
   if ((flags & FVA_TRACE) && !trace) return FVA_ERR_INVALID_ARG;
@@ -123,7 +126,7 @@ fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_d
   const fva_status s = check_shape(desc, tiling, &nb);
   if (s != FVA_OK) return s;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return FVA_ERR_INVALID_ARG;
-  const size_t need = fva::attn_workspace_bytes(desc->batch, desc->heads, nb);
+  const size_t need = fva::attn_workspace_bytes(desc->batch, desc->heads, nb, flags);
   if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;
   fva::AttnArgs a;
   a.Q = Q;

@@ -41,7 +41,8 @@ struct AttnArgs {
 };
 
 size_t route_workspace_bytes(int batch, int heads, int nb);
-size_t attn_workspace_bytes(int batch, int heads, int nb);
+size_t attn_workspace_bytes(int batch, int heads, int nb, uint32_t flags);
+int64_t attn_trace_words(int batch, int heads, int nb);
 
 hipError_t launch_route(const RouteArgs& a);
 hipError_t launch_attn(const AttnArgs& a);

@@ -57,12 +57,21 @@ def test_workspace_sizes():
     # then the fp64 score rows
     assert fva.fva_route_workspace_size(desc(), T720) == 2 * 40 * 672 * 128 * 8 + 40 * nb * nb * 8
     al = lambda x: (x + 255) // 256 * 256
-    # counts, kept lists, queue items, 9 queue bases, 8 queue counters, per-head plan scratch,
-    # one 32-byte record per block
     heads = 40
-    expect = al(rows * 4) + al(rows * nb * 4) + al(rows * 4) + al(9 * 4) + al(8 * 4) + al(heads * 19 * 4) + al(nb * 32)
-    assert fva.fva_attn_workspace_size(desc(), T720) == expect
-    assert fva.fva_trace_words(desc(), T720) == rows * 4
+    part = 66560  # one chunk's partial result: 128 x 128 fp32 O, 128 references, 128 sums
+
+    def attn_ws(cap):
+        # counts, kept lists, queue items (rows + chunks), 9 queue bases, 8 queue
+        # counters, per-head plan scratch, per-row prefixes, split count, chunk and
+        # split records, partial results, one 32-byte record per block
+        return (al(rows * 4) + al(rows * nb * 4) + al((rows + cap) * 4) + al(9 * 4) + al(8 * 4)
+                + al(heads * 19 * 4) + al(3 * (rows + 1) * 4) + al(4) + 2 * al(cap * 16) + al(cap * part)
+                + al(nb * 32))
+
+    assert fva.fva_attn_workspace_size(desc(), T720) == attn_ws(2048)
+    assert fva.fva_attn_workspace_size(desc(), T720, fva.FVA_SCHED_NAIVE) == attn_ws(0)
+    assert fva.fva_attn_workspace_size(desc(), T720, fva.FVA_SPLIT_BLOCKS(200)) == attn_ws(rows * 4)
+    assert fva.fva_trace_words(desc(), T720) == (rows + 2048) * 4
 
 
 @pytest.mark.parametrize(
@@ -113,6 +122,7 @@ def _attn(flags=0, counts=None, kv=None, mask=FAKE, trace=None, scale=0.0, ws=FA
 
 def test_attn_argument_errors():
     assert _attn(flags=8) == fva.FVA_ERR_INVALID_ARG
+    assert _attn(flags=1 << 24) == fva.FVA_ERR_INVALID_ARG  # beyond the chunk-size field
     assert _attn(counts=FAKE, kv=None) == fva.FVA_ERR_INVALID_ARG
     assert _attn(counts=None, kv=FAKE) == fva.FVA_ERR_INVALID_ARG
     assert _attn(mask=None) == fva.FVA_ERR_INVALID_ARG

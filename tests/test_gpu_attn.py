@@ -186,8 +186,10 @@ def test_attn_deterministic_and_trace():
     torch.cuda.synchronize()
     assert torch.equal(O1, O2) and torch.equal(O1, O3)
     tr = trace.view(-1, 4).cpu().numpy()
-    assert tr.shape[0] == cfg.heads * geo.nb
-    assert np.all(tr[:, 1] >= tr[:, 0]) and np.all(tr[:, 0] > 0)
+    rows = cfg.heads * geo.nb
+    assert tr.shape[0] == rows + 2048  # rows, then chunk records (no row is split here)
+    assert np.all(tr[:rows, 1] >= tr[:rows, 0]) and np.all(tr[:rows, 0] > 0)
+    assert not tr[rows:].any()
 
 
 def test_attn_max_blocks_sampled():
@@ -221,3 +223,74 @@ def test_attn_batch_two_odd_heads():
     torch = torch_mod()
     assert torch.equal(O_p, O_n) and torch.equal(O_p, O_m)
     compare_full("batch2", Qb, Kb, Vb, cfg, mask.cpu().numpy(), o64(O_p))
+
+
+@pytest.mark.parametrize("s", [1, 2, 3, 5])
+@pytest.mark.parametrize("grid,tile", [((3, 16, 16), (1, 8, 8)), ((5, 13, 21), (2, 8, 8))])
+def test_attn_split_forced(s, grid, tile):
+    # Every row keeping more than s blocks runs as ceil(count / s) chunk items
+    # on different workgroups; combine_kernel merges their partial results in
+    # chunk order, so the output is deterministic and within the bar.
+    torch = torch_mod()
+    fva = lib()
+    cfg = custom_config("split", 2, grid, tile, (0.5, 3.0), seed=23)
+    geo = geometry_of(cfg)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    mask = make_mask("random70", 1, 2, geo.nb, geo, np.random.default_rng(s))
+    mask[..., ::4, :] = 0  # some empty rows too
+    q, k, v = upload(Qb, Kb, Vb)
+    mt = torch.from_numpy(mask).to("cuda:0")
+    O1 = run_attn(q, k, v, cfg, mt, flags=fva.FVA_SPLIT_BLOCKS(s))
+    O2 = run_attn(q, k, v, cfg, mt, flags=fva.FVA_SPLIT_BLOCKS(s))
+    assert torch.equal(O1, O2)
+    O_whole = run_attn(q, k, v, cfg, mt)
+    d = (O1.float() - O_whole.float()).abs().max().item()
+    log(f"[attn] split s={s} grid{grid}: max |split - whole| {d:.3e}")
+    compare_full(f"split s={s} grid{grid}", Qb, Kb, Vb, cfg, mask, o64(O1))
+
+
+def test_attn_split_routed_tiny():
+    fva = lib()
+    cfg = synth.get_config("tiny")
+    Qb, Kb, Vb = workload("tiny")
+    q, k, v = upload(Qb, Kb, Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    O = run_attn(q, k, v, cfg, mask, counts, kv, flags=fva.FVA_SPLIT_BLOCKS(2))
+    compare_full("tiny split s=2", Qb, Kb, Vb, cfg, mask.cpu().numpy(), o64(O))
+
+
+def test_attn_split_automatic_one_head():
+    # One flat head of the 480p shape: 308 query blocks for the 512 workgroup
+    # slots, ~250 kept blocks a row. The automatic chunk size
+    # max(32, ceil(total / 1024)) splits the long rows; the trace shows chunk
+    # items, and sampled rows match the oracle.
+    torch = torch_mod()
+    fva = lib()
+    cfg = custom_config("one_head", 1, (21, 30, 52), (2, 8, 8), (0.5,), seed=24)
+    geo = geometry_of(cfg)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    q, k, v = upload(Qb, Kb, Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    c = counts.cpu().numpy()[0, 0]
+    total = int((c + 1).sum())
+    S = max(32, -(-total // 1024))
+    n_chunks = int(sum(-(-x // S) for x in c if x > S))
+    assert n_chunks > 0
+    desc = fva._desc_of(q)
+    trace = torch.zeros(fva.fva_trace_words(desc, tiling_of(cfg)), dtype=torch.int64, device="cuda:0")
+    O = fva.fva_attn(q, k, v, tiling_of(cfg), mask, counts, kv, flags=fva.FVA_TRACE, trace=trace)
+    torch.cuda.synchronize()
+    tr = trace.view(-1, 4).cpu().numpy()
+    rows = geo.nb
+    split_rows = c > S
+    assert np.all(tr[:rows][~split_rows, 0] > 0) and not tr[:rows][split_rows].any()
+    assert np.all(tr[rows:rows + n_chunks, 0] > 0) and not tr[rows + n_chunks:].any()
+    O_naive = run_attn(q, k, v, cfg, mask, counts, kv, flags=fva.FVA_SCHED_NAIVE)
+    log(f"[attn] one head: S={S}, {split_rows.sum()} rows split into {n_chunks} chunks, "
+        f"max |split - whole| {(O.float() - O_naive.float()).abs().max().item():.3e}")
+    m = mask.cpu().numpy()[0, 0]
+    sample = sorted(set([int(i) for i in np.nonzero(split_rows)[0][:12]] + [0, rows - 1]))
+    ref = attn_ref_rows(f64(Qb[0, 0]), f64(Kb[0, 0]), f64(Vb[0, 0]), m, geo, sample)
+    Of = O[0, 0].float().cpu().numpy()
+    e = np.concatenate([np.abs(Of[geo.block_tokens[i]] - o).ravel() for i, o in ref.items()])
+    assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
