@@ -69,26 +69,32 @@ def source_digest(*paths):
 def imbalance(trace, counts):
     """Per-CU and per-XCD load figures from an FVA_TRACE record.
 
-    CU = (xcc, bits 8.. of HW_ID); busy = sum of item durations on the CU.
-    rho = max/mean over XCDs of summed kept blocks (Eq. 2 with XCDs as ranks)
-    and of summed item time.
+    Records: one per (b, h, i) row, then one per chunk item of a split row
+    (a split row's own record stays empty). CU = (xcc, bits 8.. of HW_ID);
+    busy = sum of item durations on the CU. rho = max/mean over XCDs of summed
+    item time, and of summed kept blocks over the unsplit rows (Eq. 2 with
+    XCDs as ranks).
     """
     tr = trace.reshape(-1, 4)
-    dur = (tr[:, 1] - tr[:, 0]).astype(np.float64)
-    loc = tr[:, 2]
+    rows = counts.size
+    used = tr[:, 0] > 0
+    dur = (tr[:, 1] - tr[:, 0]).astype(np.float64)[used]
+    loc = tr[used, 2]
     cu = loc >> 8
     xcc = loc >> 16
-    cost = counts.reshape(-1).astype(np.float64)
     _, inv = np.unique(cu, return_inverse=True)
     busy = np.bincount(inv, weights=dur)
     xb = np.bincount(xcc, weights=dur, minlength=8)
-    xc = np.bincount(xcc, weights=cost, minlength=8)
-    span = float(tr[:, 1].max() - tr[:, 0].min()) / 100.0  # 100 MHz clock -> us
+    row_used = used[:rows]
+    xc = np.bincount(tr[:rows, 2][row_used] >> 16, weights=counts.reshape(-1)[row_used].astype(np.float64),
+                     minlength=8)
+    span = float(tr[used, 1].max() - tr[used, 0].min()) / 100.0  # 100 MHz clock -> us
     return {
         "cus_used": int(busy.size),
         "cu_busy_max_over_mean": round(float(busy.max() / busy.mean()), 4),
         "xcd_time_rho": round(float(xb.max() / xb.mean()), 4),
         "xcd_blocks_rho": round(float(xc.max() / xc.mean()), 4),
+        "chunk_items": int(used[rows:].sum()),
         "span_us": round(span, 1),
     }
 

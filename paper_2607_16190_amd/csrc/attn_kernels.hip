@@ -639,25 +639,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
   }
 }
 
-// Exclusive prefix over the 1024 threads of a workgroup of one int per
-// thread; *total gets the sum. wsum: LDS scratch of 16 ints.
-__device__ __forceinline__ int block_excl_scan(int v, int* wsum, int* total) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int incl = wave_incl_scan_i32(v, lane);
-  if (lane == 63) wsum[wave] = incl;
-  __syncthreads();
-  int before = 0, all = 0;
-  for (int w = 0; w < 16; ++w) {
-    const int t = wsum[w];
-    before += w < wave ? t : 0;
-    all += t;
-  }
-  __syncthreads();
-  *total = all;
-  return before + incl - v;
-}
-
 constexpr int kMinChunk = 32;  // smallest automatic chunk (kept blocks)
 
 // Builds the work list (one workgroup of 1024 threads).
@@ -680,14 +661,13 @@ constexpr int kMinChunk = 32;  // smallest automatic chunk (kept blocks)
 // (their kept K/V blocks overlap in L2).
 //
 // Scratch: per head cost, rank, run starts [kQueues + 1], queue offsets
-// [kQueues]; per row the exclusive prefixes of items, chunks and split rows.
+// [kQueues]; per row the exclusive prefixes of chunks and split rows.
 __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ counts, int n_heads, Geometry g,
                                                    int slots, int forced, int chunk_cap, int32_t* __restrict__ items,
                                                    int32_t* __restrict__ qbase, int32_t* __restrict__ qctr,
                                                    int32_t* __restrict__ hscratch, int32_t* __restrict__ rscratch,
                                                    int4* __restrict__ chunks, int4* __restrict__ splits,
                                                    int32_t* __restrict__ n_split) {
-  __shared__ int wsum[16];
   __shared__ long long wtot[16];
   const int nb = g.nb;
   const int rows = n_heads * nb;
@@ -695,8 +675,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   int32_t* horder = hcost + n_heads;
   int32_t* hstart = horder + n_heads;                  // [n_heads][kQueues + 1]
   int32_t* hoff = hstart + (size_t)n_heads * (kQueues + 1);  // [n_heads][kQueues]
-  int32_t* ipre = rscratch;                            // [rows + 1] items before row r
-  int32_t* cpre = ipre + rows + 1;                     // [rows + 1] chunks before row r
+  int32_t* cpre = rscratch;                            // [rows + 1] chunks before row r
   int32_t* spre = cpre + rows + 1;                     // [rows + 1] split rows before row r
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -716,51 +695,60 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   __syncthreads();
   long long total = 0;
   for (int w = 0; w < nwaves; ++w) total += wtot[w];
+  __syncthreads();  // wtot is reused below; every wave holds the same total
   int S = forced > 0 ? forced : (int)max((long long)kMinChunk, (total + 2LL * slots - 1) / (2LL * slots));
 
-  // 1. items per row (1, or its chunks) and the three exclusive prefixes,
-  //    each thread taking a contiguous run of rows
-  const int seg = (rows + (int)blockDim.x - 1) / (int)blockDim.x;
-  const int r0 = min((int)threadIdx.x * seg, rows);
-  const int r1 = min(r0 + seg, rows);
-  for (int attempt = 0; attempt < 2; ++attempt) {
-    auto nchunks = [&](int r) {
-      const int c = kept_of(r);
-      return c > S ? (c + S - 1) / S : 1;
-    };
-    int li = 0, lc = 0, ls = 0;
-    for (int r = r0; r < r1; ++r) {
-      const int n = nchunks(r);
-      li += n;
-      lc += n > 1 ? n : 0;
-      ls += n > 1 ? 1 : 0;
+  // 1. items per row (1, or its chunks): when no row can exceed S (the usual
+  //    case with many rows per slot) item r is row r and nothing else is
+  //    built. Otherwise one pass over tiles of 1024 rows scans, packed in one
+  //    64-bit word, the chunks (low half) and split rows (high half) before
+  //    every row; the items before row r are r + chunks - split rows.
+  const bool may_split = S < nb;
+  if (may_split) {
+    for (int attempt = 0; attempt < 2; ++attempt) {
+      auto packed = [&](int r) -> uint64_t {
+        if (r >= rows) return 0ull;
+        const int c = kept_of(r);
+        return c > S ? ((uint64_t)1 << 32) | (uint64_t)((c + S - 1) / S) : 0ull;
+      };
+      uint64_t run = 0;  // over the tiles before this one
+      for (int base = 0; base < rows; base += 1024) {
+        const int r = base + (int)threadIdx.x;
+        const uint64_t v = packed(r);
+        const uint64_t incl = wave_incl_scan_u64(v, lane);
+        if (lane == 63) wtot[wave] = (long long)incl;
+        __syncthreads();
+        uint64_t before = run, all = run;
+        for (int w = 0; w < nwaves; ++w) {
+          const uint64_t t = (uint64_t)wtot[w];
+          before += w < wave ? t : 0ull;
+          all += t;
+        }
+        __syncthreads();
+        if (r < rows) {
+          const uint64_t ex = before + incl - v;
+          cpre[r] = (int)(uint32_t)ex;
+          spre[r] = (int)(ex >> 32);
+        }
+        run = all;
+      }
+      if ((int)(uint32_t)run > chunk_cap && attempt == 0) {
+        S = 0x7fffffff;  // nothing is split
+        continue;
+      }
+      if (threadIdx.x == 0) {
+        cpre[rows] = (int)(uint32_t)run;
+        spre[rows] = (int)(run >> 32);
+        *n_split = (int)(run >> 32);
+      }
+      break;
     }
-    int ti, tc, ts;
-    int bi = block_excl_scan(li, wsum, &ti);
-    int bc = block_excl_scan(lc, wsum, &tc);
-    int bs = block_excl_scan(ls, wsum, &ts);
-    if (tc > chunk_cap && attempt == 0) {
-      S = 0x7fffffff;  // nothing is split
-      continue;
-    }
-    for (int r = r0; r < r1; ++r) {
-      const int n = nchunks(r);
-      ipre[r] = bi;
-      cpre[r] = bc;
-      spre[r] = bs;
-      bi += n;
-      bc += n > 1 ? n : 0;
-      bs += n > 1 ? 1 : 0;
-    }
-    if (threadIdx.x == 0) {
-      ipre[rows] = ti;
-      cpre[rows] = tc;
-      spre[rows] = ts;
-      *n_split = ts;
-    }
-    break;
+  } else if (threadIdx.x == 0) {
+    *n_split = 0;
   }
   __syncthreads();
+  // items before row r (ipre[r])
+  auto ipre = [&](int r) { return may_split ? r + cpre[r] - spre[r] : r; };
 
   // 2. head costs and equal-cost runs (one wave per head)
   for (int h = wave; h < n_heads; h += nwaves) {
@@ -817,7 +805,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
       const int h = horder[r];
       const int32_t* st = hstart + (size_t)h * (kQueues + 1);
       hoff[(size_t)h * kQueues + x] = run;
-      run += ipre[h * nb + st[x + 1]] - ipre[h * nb + st[x]];
+      run += ipre(h * nb + st[x + 1]) - ipre(h * nb + st[x]);
     }
     qctr[x] = run;  // queue length for now
   }
@@ -841,8 +829,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
     const int32_t* st = hstart + (size_t)h * (kQueues + 1);
     int x = 0;
     while (x + 1 < kQueues && st[x + 1] <= i) ++x;
-    const int pos = qbase[x] + hoff[(size_t)h * kQueues + x] + (ipre[r] - ipre[h * nb + st[x]]);
-    const int n = ipre[r + 1] - ipre[r];
+    const int pos = qbase[x] + hoff[(size_t)h * kQueues + x] + (ipre(r) - ipre(h * nb + st[x]));
+    const int n = ipre(r + 1) - ipre(r);
     if (n == 1) {
       items[pos] = r;
     } else {
@@ -962,7 +950,7 @@ struct AttnWorkspace {
   int32_t* qbase;    // [kQueues + 1]
   int32_t* qctr;     // [kQueues]
   int32_t* hscratch; // [heads * (2 + 2 * kQueues + 1)]
-  int32_t* rscratch; // [3 * (rows + 1)] per-row prefixes
+  int32_t* rscratch; // [2 * (rows + 1)] per-row prefixes
   int32_t* n_split;  // [1]
   int4* chunks;      // [cap]
   int4* splits;      // [cap]
@@ -1007,7 +995,7 @@ AttnWorkspace carve(void* base, int batch, int heads, int nb, uint32_t flags) {
   w.hscratch = reinterpret_cast<int32_t*>(p + off);
   off += al(nh * (2 + 2 * kQueues + 1) * 4);
   w.rscratch = reinterpret_cast<int32_t*>(p + off);
-  off += al(3 * (rows + 1) * 4);
+  off += al(2 * (rows + 1) * 4);
   w.n_split = reinterpret_cast<int32_t*>(p + off);
   off += al(4);
   w.chunks = reinterpret_cast<int4*>(p + off);

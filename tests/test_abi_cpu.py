@@ -65,7 +65,7 @@ def test_workspace_sizes():
         # counters, per-head plan scratch, per-row prefixes, split count, chunk and
         # split records, partial results, one 32-byte record per block
         return (al(rows * 4) + al(rows * nb * 4) + al((rows + cap) * 4) + al(9 * 4) + al(8 * 4)
-                + al(heads * 19 * 4) + al(3 * (rows + 1) * 4) + al(4) + 2 * al(cap * 16) + al(cap * part)
+                + al(heads * 19 * 4) + al(2 * (rows + 1) * 4) + al(4) + 2 * al(cap * 16) + al(cap * part)
                 + al(nb * 32))
 
     assert fva.fva_attn_workspace_size(desc(), T720) == attn_ws(2048)
