@@ -153,11 +153,11 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0):
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each scaled by the factor the same
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
-ATTN_TRAFFIC = {"source_digest": "477d15bf4055128b", "workload": "720p", "bytes": (115500613 * 2 + 757141) * 1024}
+ATTN_TRAFFIC = {"source_digest": "3b109d3a92d8d49c", "workload": "720p", "bytes": (110849142 * 2 + 757118) * 1024}
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call on
 # the 720p workload (FETCH x 2, WRITE x 1, KiB per dispatch summed).
-ROUTE_TRAFFIC = {"source_digest": "66511eaf26a3a2f0", "workload": "720p",
-                 "bytes": ((756165 + 29490 + 68205) * 2 + 53760 + 138159 + 49288) * 1024}
+ROUTE_TRAFFIC = {"source_digest": "dc7373a9a05f796c", "workload": "720p",
+                 "bytes": ((756165 + 29465 + 68194) * 2 + 53760 + 138774 + 49288) * 1024}
 
 
 def copy_calibration(torch, gib=1.0, reps=5):
