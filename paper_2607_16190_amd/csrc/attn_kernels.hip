@@ -639,7 +639,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
   }
 }
 
-constexpr int kMinChunk = 32;  // smallest automatic chunk (kept blocks)
+constexpr int kMinChunk = 32;      // smallest automatic chunk (kept blocks)
+constexpr int kPlanLdsHeads = 1024;  // heads whose queue bookkeeping the plan keeps in LDS
 
 // Builds the work list (one workgroup of 1024 threads).
 //
@@ -669,6 +670,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
                                                    int4* __restrict__ chunks, int4* __restrict__ splits,
                                                    int32_t* __restrict__ n_split) {
   __shared__ long long wtot[16];
+  __shared__ int lds_order[kPlanLdsHeads];
+  __shared__ int lds_len[kPlanLdsHeads * kQueues];
   const int nb = g.nb;
   const int rows = n_heads * nb;
   int32_t* hcost = hscratch;
@@ -797,15 +800,35 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   }
   __syncthreads();
 
-  // 4. queue offsets (in items) of every (head, run) and queue bases
+  // 4. queue offsets (in items) of every (head, run) and queue bases: a
+  //    walk over the heads in cost order, from LDS copies of the order and
+  //    of the item count of every (head, run) when they fit
+  const bool in_lds = n_heads <= kPlanLdsHeads;
+  if (in_lds) {
+    for (int r = threadIdx.x; r < n_heads; r += blockDim.x) {
+      const int h = horder[r];
+      const int32_t* st = hstart + (size_t)h * (kQueues + 1);
+      lds_order[r] = h;
+#pragma unroll
+      for (int x = 0; x < kQueues; ++x) lds_len[r * kQueues + x] = ipre(h * nb + st[x + 1]) - ipre(h * nb + st[x]);
+    }
+    __syncthreads();
+  }
   if (threadIdx.x < kQueues) {
     const int x = threadIdx.x;
     int run = 0;
     for (int r = 0; r < n_heads; ++r) {
-      const int h = horder[r];
-      const int32_t* st = hstart + (size_t)h * (kQueues + 1);
+      int h, len;
+      if (in_lds) {
+        h = lds_order[r];
+        len = lds_len[r * kQueues + x];
+      } else {
+        h = horder[r];
+        const int32_t* st = hstart + (size_t)h * (kQueues + 1);
+        len = ipre(h * nb + st[x + 1]) - ipre(h * nb + st[x]);
+      }
       hoff[(size_t)h * kQueues + x] = run;
-      run += ipre(h * nb + st[x + 1]) - ipre(h * nb + st[x]);
+      run += len;
     }
     qctr[x] = run;  // queue length for now
   }
@@ -822,25 +845,31 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   __syncthreads();
 
   // 5. scatter items (a split row's chunks consecutively), chunk and split
-  //    records; reset the queue counters
-  for (int r = threadIdx.x; r < rows; r += blockDim.x) {
-    const int h = r / nb;
-    const int i = r - h * nb;
+  //    records; one wave per head, whose run x fills one contiguous slice of
+  //    queue x. Then reset the queue counters.
+  for (int h = wave; h < n_heads; h += nwaves) {
     const int32_t* st = hstart + (size_t)h * (kQueues + 1);
-    int x = 0;
-    while (x + 1 < kQueues && st[x + 1] <= i) ++x;
-    const int pos = qbase[x] + hoff[(size_t)h * kQueues + x] + (ipre(r) - ipre(h * nb + st[x]));
-    const int n = ipre(r + 1) - ipre(r);
-    if (n == 1) {
-      items[pos] = r;
-    } else {
-      const int c0 = cpre[r];
-      const int cnt = kept_of(r);
-      for (int c = 0; c < n; ++c) {
-        items[pos + c] = -1 - (c0 + c);
-        chunks[c0 + c] = make_int4(r, (int)(((int64_t)c * cnt) / n), (int)(((int64_t)(c + 1) * cnt) / n), 0);
+    for (int x = 0; x < kQueues; ++x) {
+      const int i_begin = __builtin_amdgcn_readfirstlane(st[x]);
+      const int i_end = __builtin_amdgcn_readfirstlane(st[x + 1]);
+      if (i_begin >= i_end) continue;
+      const int slice = qbase[x] + hoff[(size_t)h * kQueues + x] - ipre(h * nb + i_begin);
+      for (int i = i_begin + lane; i < i_end; i += 64) {
+        const int r = h * nb + i;
+        const int pos = slice + ipre(r);
+        const int n = ipre(r + 1) - ipre(r);
+        if (n == 1) {
+          items[pos] = r;
+        } else {
+          const int c0 = cpre[r];
+          const int cnt = kept_of(r);
+          for (int c = 0; c < n; ++c) {
+            items[pos + c] = -1 - (c0 + c);
+            chunks[c0 + c] = make_int4(r, (int)(((int64_t)c * cnt) / n), (int)(((int64_t)(c + 1) * cnt) / n), 0);
+          }
+          splits[spre[r]] = make_int4(r, c0, n, 0);
+        }
       }
-      splits[spre[r]] = make_int4(r, c0, n, 0);
     }
   }
   __syncthreads();
