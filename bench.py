@@ -153,7 +153,7 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0):
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each scaled by the factor the same
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
-ATTN_TRAFFIC = {"source_digest": "3b109d3a92d8d49c", "workload": "720p", "bytes": (110849142 * 2 + 757118) * 1024}
+ATTN_TRAFFIC = {"source_digest": "21ec65e63b649c4f", "workload": "720p", "bytes": (111515775 * 2 + 757113) * 1024}
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call on
 # the 720p workload (FETCH x 2, WRITE x 1, KiB per dispatch summed).
 ROUTE_TRAFFIC = {"source_digest": "dc7373a9a05f796c", "workload": "720p",
