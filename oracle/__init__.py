@@ -10,7 +10,8 @@ Passages followed (FVAttn, "Adaptive Sparse Attention with Runtime Load
 Balancing for Video Generation"):
 
 * video-aware block organisation and pooled block similarities -- §3.1
-  (routing frontend paragraph);
+  (routing frontend paragraph), as 3D boxes or as runs of a Hilbert curve
+  (the block reordering of the same paragraph);
 * block mask M_{h,i,j} over (query block, key block) pairs -- §2.1;
 * Top-p: the smallest set of key blocks whose cumulative normalised
   importance reaches p -- §2.1;
@@ -26,6 +27,7 @@ checkable against the paper's numbers.
 """
 
 from .tiling import TileGeometry, tile_geometry
+from .curve import curve_bits, hilbert_index, curve_order, curve_geometry
 from .route import (
     pool_blocks,
     block_scores,
@@ -39,6 +41,10 @@ from .attention import attn_ref_rows, attn_ref_head
 __all__ = [
     "TileGeometry",
     "tile_geometry",
+    "curve_bits",
+    "hilbert_index",
+    "curve_order",
+    "curve_geometry",
     "pool_blocks",
     "block_scores",
     "block_softmax",

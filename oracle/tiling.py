@@ -34,7 +34,8 @@ class TileGeometry:
     nbx: int
     block_of_token: np.ndarray  # int64 [N]: block id of every token
     block_sizes: np.ndarray  # int64 [nb]: real tokens per block
-    block_tokens: tuple  # nb arrays of ascending token ids
+    block_tokens: tuple  # nb arrays of token ids (ascending for boxes, curve order otherwise)
+    order: str = "box"  # "box": 3D boxes; "hilbert": runs of a Hilbert curve (oracle.curve)
 
     @property
     def N(self) -> int:
