@@ -13,7 +13,13 @@ Beside it: attention ms, route us and route GB/s, kept-tile TFLOPS
 retained fraction, a roofline object for the attention kernel and the fp64
 CPU oracle timed on a bounded sample.
 
-    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--workload 720p]
+    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--workload 720p] [--blocks box|hilbert]
+
+--blocks hilbert runs the same inputs with the Hilbert-curve block
+organisation: Q, K, V are permuted into curve order once before timing (the
+permutation and the curve order are timed on their own and reported), and
+the step routes and attends on the curve-ordered tensors with blocks of
+bt*bh*bw consecutive curve positions.
 """
 
 import argparse
@@ -99,13 +105,16 @@ def imbalance(trace, counts):
     }
 
 
-def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0):
+def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
     """Oracle timed on this host on a bounded sample; returns dict."""
-    from oracle import attn_ref_rows, route_ref, tile_geometry
+    from oracle import attn_ref_rows, curve_geometry, route_ref, tile_geometry
 
     import synth
 
-    geo = tile_geometry(*cfg.grid, *cfg.tile)
+    if blocks == "hilbert":
+        geo = curve_geometry(*cfg.grid, int(np.prod(cfg.tile)))
+    else:
+        geo = tile_geometry(*cfg.grid, *cfg.tile)
     cores = len(os.sched_getaffinity(0))
     f64 = lambda b: synth.bf16_bits_to_f32(b).astype(np.float64)
     H = cfg.heads
@@ -149,15 +158,26 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0):
     }
 
 
-# HBM bytes per launch of attn_persistent_kernel on the 720p workload from
-# rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each scaled by the factor the same
+# HBM bytes per launch of attn_persistent_kernel on the 720p workload (3D
+# boxes, and Hilbert-curve blocks) from rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each scaled by the factor the same
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
-ATTN_TRAFFIC = {"source_digest": "21ec65e63b649c4f", "workload": "720p", "bytes": (111515775 * 2 + 757113) * 1024}
-# Same for fva_route (pool_kernel + score_kernel + select_kernel), per call on
-# the 720p workload (FETCH x 2, WRITE x 1, KiB per dispatch summed).
-ROUTE_TRAFFIC = {"source_digest": "dc7373a9a05f796c", "workload": "720p",
-                 "bytes": ((756165 + 29465 + 68194) * 2 + 53760 + 138774 + 49288) * 1024}
+ATTN_TRAFFIC = {
+    "source_digest": "2e8cc5e63181d037",
+    "bytes": {
+        "720p": (112363341 * 2 + 757141) * 1024,
+        "720p-hilbert": (89289480 * 2 + 757163) * 1024,
+    },
+}
+# Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
+# (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
+ROUTE_TRAFFIC = {
+    "source_digest": "4a6577e51f087d77",
+    "bytes": {
+        "720p": ((756175 + 29422 + 68204) * 2 + 53760 + 138978 + 49287) * 1024,
+        "720p-hilbert": ((756146 + 25769 + 55008) * 2 + 47360 + 112266 + 39990) * 1024,
+    },
+}
 
 
 def copy_calibration(torch, gib=1.0, reps=5):
@@ -179,6 +199,39 @@ def copy_calibration(torch, gib=1.0, reps=5):
                       "copy_GBps_read_plus_write": 2 * n / t / 1e9}), flush=True)
 
 
+def curve_setup(torch, fva, cfg, q, k, v, reps=5):
+    """Curve order and curve-ordered copies of q, k, v; times both (HIP events, mean of reps)."""
+    T, H, W = cfg.grid
+    stream = torch.cuda.current_stream()
+    ws = torch.empty(fva.fva_curve_workspace_size(T, H, W), dtype=torch.uint8, device=q.device)
+    perm = fva.fva_curve_order(T, H, W, device=q.device, workspace=ws)
+    qc, kc, vc = (fva.fva_permute_tokens(x, perm, fva.FVA_TO_CURVE) for x in (q, k, v))
+    o = torch.empty_like(q)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ev[0].record(stream)
+    for _ in range(reps):
+        fva.fva_curve_order(T, H, W, out=perm, workspace=ws)
+    ev[1].record(stream)
+    for _ in range(reps):
+        for x, y in ((q, qc), (k, kc), (v, vc)):
+            fva.fva_permute_tokens(x, perm, fva.FVA_TO_CURVE, out=y)
+        fva.fva_permute_tokens(qc, perm, fva.FVA_FROM_CURVE, out=o)
+    ev[2].record(stream)
+    torch.cuda.synchronize()
+    t_order = ev[0].elapsed_time(ev[1]) / reps * 1e3
+    t_perm = ev[1].elapsed_time(ev[2]) / reps * 1e3
+    moved = 4 * 2 * q.numel() * 2  # four tensors, each read and written once
+    del o
+    return {
+        "qkv": (qc, kc, vc),
+        "curve_order_us": round(t_order, 1),
+        "permute_qkv_in_o_out_us": round(t_perm, 1),
+        "permute_GBps": round(moved / (t_perm / 1e6) / 1e9, 1),
+        "note": "done once per grid / per model call, outside the timed step",
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -188,6 +241,8 @@ def main():
     ap.add_argument("--p", type=float, default=None)
     ap.add_argument("--p-sweep", default=None, help="comma-separated p values, timed after the main run")
     ap.add_argument("--sched", choices=["persistent", "naive"], default="persistent")
+    ap.add_argument("--blocks", choices=["box", "hilbert"], default="box",
+                    help="3D boxes, or runs of the Hilbert curve over curve-ordered tokens")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true", help="skip the scheduler imbalance trace runs")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
@@ -213,13 +268,25 @@ def main():
 
     cfg = synth.get_config(args.workload)
     p = cfg.p if args.p is None else args.p
-    tiling = fva.Tiling(*cfg.grid, *cfg.tile)
-    sizes = block_sizes(cfg.grid, cfg.tile)
     dev = torch.device("cuda:0")
     log(f"[bench] generating {cfg.name}: {cfg.heads} heads x {cfg.N} tokens x 128")
     Qb, Kb, Vb = synth.gen_qkv(cfg)
     up = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
     q, k, v = up(Qb), up(Kb), up(Vb)
+    curve = None
+    if args.blocks == "hilbert":
+        blk = int(np.prod(cfg.tile))
+        tiling = fva.Tiling.curve(cfg.N, blk)
+        nb_c = -(-cfg.N // blk)
+        sizes = np.full(nb_c, blk, dtype=np.int64)
+        sizes[-1] = cfg.N - blk * (nb_c - 1)
+        curve = curve_setup(torch, fva, cfg, q, k, v)
+        q, k, v = curve.pop("qkv")
+        log(f"[bench] curve order {curve['curve_order_us']} us, permute Q,K,V in + O out "
+            f"{curve['permute_qkv_in_o_out_us']} us")
+    else:
+        tiling = fva.Tiling(*cfg.grid, *cfg.tile)
+        sizes = block_sizes(cfg.grid, cfg.tile)
     desc = fva._desc_of(q)
     nb = fva.fva_num_blocks(tiling)
     assert nb == sizes.shape[0]
@@ -276,12 +343,13 @@ def main():
     shared = [os.path.join(csrc, f) for f in ("fva_common.h", "fva_geometry.h")]
     digest = source_digest(os.path.join(csrc, "attn_kernels.hip"), *shared)
     traffic = None
-    if ATTN_TRAFFIC["source_digest"] == digest and ATTN_TRAFFIC["workload"] == cfg.name and args.sched == "persistent":
-        traffic = ATTN_TRAFFIC["bytes"]
+    bench_workload = cfg.name if curve is None else cfg.name + "-hilbert"
+    if ATTN_TRAFFIC["source_digest"] == digest and args.sched == "persistent":
+        traffic = ATTN_TRAFFIC["bytes"].get(bench_workload)
     route_digest = source_digest(os.path.join(csrc, "route_kernels.hip"), *shared)
     route_traffic = None
-    if ROUTE_TRAFFIC["source_digest"] == route_digest and ROUTE_TRAFFIC["workload"] == cfg.name:
-        route_traffic = ROUTE_TRAFFIC["bytes"]
+    if ROUTE_TRAFFIC["source_digest"] == route_digest:
+        route_traffic = ROUTE_TRAFFIC["bytes"].get(bench_workload)
     res = {
         "metric": METRIC,
         "value": round(dense_flops / (ms_per_step / 1e3) / 1e12, 2),
@@ -297,7 +365,10 @@ def main():
         "data": "synthetic (seeded video-shaped Q/K/V, sinusoidal (t,y,x) embedding, per-head alpha)",
         "config": {
             "workload": f"{cfg.name}: {H} heads, d=128, latent grid {'x'.join(map(str, cfg.grid))} = {N} tokens, "
-            f"tile {'x'.join(map(str, cfg.tile))}, nb={nb}, p={p}, k_min={cfg.k_min}",
+            + (f"tile {'x'.join(map(str, cfg.tile))}" if curve is None
+               else f"Hilbert-curve blocks of {int(np.prod(cfg.tile))} tokens")
+            + f", nb={nb}, p={p}, k_min={cfg.k_min}",
+            "blocks": args.blocks,
             "batch": B,
             "heads": H,
             "tokens": N,
@@ -336,6 +407,8 @@ def main():
             "attn_source_digest": digest,
         },
     }
+    if curve is not None:
+        res["curve_layout"] = curve
     if not args.no_trace:
         tw = fva.fva_trace_words(desc, tiling)
         trace = torch.zeros(tw, dtype=torch.int64, device=dev)
@@ -360,7 +433,7 @@ def main():
         res["p_sweep"] = sweep
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
-        res["cpu_baseline"] = cpu_baseline(cfg, Qb, Kb, Vb, m_np, c_np, args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(cfg, Qb, Kb, Vb, m_np, c_np, args.cpu_budget, args.blocks)
     print(json.dumps(res), flush=True)
 
 

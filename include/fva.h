@@ -6,7 +6,8 @@
  * ("Adaptive Sparse Attention with Runtime Load Balancing for Video
  * Generation"): the routing frontend of §3.1 (video-aware 3D blocks,
  * pooled block similarities, Top-p with a Top-k floor, §2.1) and
- * block-sparse attention over the retained blocks (§2.1, §3.1).
+ * block-sparse attention over the retained blocks (§2.1, §3.1), with the
+ * Hilbert-curve block order of §3.1 as an alternative block organisation.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -51,7 +52,8 @@ typedef enum fva_status {
   FVA_OK = 0,
   FVA_ERR_INVALID_ARG = -1, /* null pointer, p outside [0,1] or NaN, k_min < 0, bad flags */
   FVA_ERR_SHAPE = -2,       /* tokens != T*H*W, non-positive extents, bad strides */
-  FVA_ERR_UNSUPPORTED = -3, /* head_dim != 128, tile volume not 64/128, nb > 1024, head > 2 GiB */
+  FVA_ERR_UNSUPPORTED = -3, /* head_dim != 128, tile volume not 64/128, nb > 1024, head > 2 GiB,
+                               curve grid extent > 256 */
   FVA_ERR_WORKSPACE = -4,   /* workspace missing or smaller than the query says */
   FVA_ERR_HIP = -5          /* a kernel launch failed */
 } fva_status;
@@ -164,6 +166,65 @@ fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_d
                     const fva_tiling* tiling, const uint8_t* block_mask, const int32_t* counts,
                     const int32_t* kv_idx, float softmax_scale, uint32_t flags, void* O, void* workspace,
                     size_t workspace_bytes, void* trace, void* stream);
+
+/*
+ * Hilbert-curve block organisation (§3.1, routing frontend: blocks are
+ * reordered along a Hilbert curve so that tokens that are close in the
+ * latent video land in nearby blocks at every scale).
+ *
+ * The curve is J. Skilling's 3D Hilbert curve ("Programming the Hilbert
+ * curve", AIP Conf. Proc. 707, 2004) on the cube of side 2^k, k the smallest
+ * integer with 2^k >= max(T, H, W); token (t, y, x) is the point with axes
+ * (0, 1, 2) = (t, y, x), axis 0 giving the most significant bit of each
+ * 3-bit digit of the curve index. The rank of a token is the number of grid
+ * tokens with a smaller curve index.
+ *
+ * Curve layout: a curve-ordered tensor holds at sequence position r the
+ * token whose rank is r. fva_route and fva_attn run on curve-ordered Q, K, V
+ * with the one-dimensional tiling {T = 1, H = 1, W = N, bt = 1, bh = 1,
+ * bw = B}, B in {64, 128}: block i is ranks [iB, min((i+1)B, N)), every
+ * block full except the last, and O comes back curve-ordered. Permuting
+ * once into curve order and once back is the caller's choice of where in
+ * its model to do it (e.g. around the whole stack of attention layers).
+ */
+#define FVA_TO_CURVE 0   /* dst[.., r, :] = src[.., perm[r], :] */
+#define FVA_FROM_CURVE 1 /* dst[.., perm[r], :] = src[.., r, :] */
+
+/* Workspace bytes of fva_curve_order: a bitmap of 8^k bits and its word
+ * prefix sums (each max(1, 8^k / 32) * 4 bytes) and one uint32 curve index
+ * per token, each part 256-byte aligned. FVA_ERR_SHAPE for a non-positive
+ * extent, FVA_ERR_UNSUPPORTED for an extent above 256. Host only. */
+fva_status fva_curve_workspace_size(int32_t T, int32_t H, int32_t W, size_t* bytes);
+
+/*
+ * fva_curve_order -- perm[r] = raster token id (t*H + y)*W + x of the token
+ * of rank r, for every r < T*H*W (device int32 [T*H*W], fully written).
+ * Exact integer work; the result depends only on (T, H, W), so a caller
+ * builds it once per grid and keeps it.
+ * workspace: at least fva_curve_workspace_size bytes of device memory,
+ *            256-byte aligned; its contents are scratch.
+ * Errors as for fva_curve_workspace_size, FVA_ERR_INVALID_ARG for a NULL
+ * perm, FVA_ERR_WORKSPACE for a missing or short workspace.
+ */
+fva_status fva_curve_order(int32_t T, int32_t H, int32_t W, int32_t* perm, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
+ * fva_permute_tokens -- moves whole token rows of a bf16 tensor with the
+ * layout of fva_qkv_desc (head_dim 128) between raster and curve order:
+ * FVA_TO_CURVE gathers dst[b,h,r,:] = src[b,h,perm[r],:], FVA_FROM_CURVE
+ * scatters dst[b,h,perm[r],:] = src[b,h,r,:], for r < desc->tokens, with
+ * perm from fva_curve_order (any permutation of 0 .. tokens-1 works). src
+ * and dst share desc's strides and must not overlap (src == dst is
+ * rejected; a partial overlap is not detected). A perm entry outside
+ * [0, tokens) is never dereferenced: the gathered row is written as zeros,
+ * the scattered row is dropped.
+ * Errors: FVA_ERR_INVALID_ARG (NULL pointer, src == dst, rows not 16-byte
+ * aligned, bad direction), FVA_ERR_SHAPE (bad extents or strides),
+ * FVA_ERR_UNSUPPORTED (head_dim != 128, batch*heads > 65535).
+ */
+fva_status fva_permute_tokens(const void* src, void* dst, const fva_qkv_desc* desc, const int32_t* perm,
+                              int32_t direction, void* stream);
 
 /* Static description of a status code. */
 const char* fva_status_string(fva_status status);

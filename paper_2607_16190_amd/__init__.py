@@ -8,6 +8,15 @@ has not been built; there is no fallback implementation.
     import paper_2607_16190_amd as fva
     mask, counts, kv_idx = fva.fva_route(q, k, 0.9, 4, fva.Tiling(21, 45, 80, 2, 8, 8))
     out = fva.fva_attn(q, k, v, tiling, mask, counts, kv_idx)
+
+Hilbert-curve blocks: permute Q, K, V into curve order once, route and
+attend with the one-dimensional tiling, and permute O back:
+
+    perm = fva.fva_curve_order(21, 45, 80, device=q.device)
+    qc, kc, vc = (fva.fva_permute_tokens(x, perm, fva.FVA_TO_CURVE) for x in (q, k, v))
+    tc = fva.Tiling.curve(21 * 45 * 80, 128)
+    oc = fva.fva_attn(qc, kc, vc, tc, *fva.fva_route(qc, kc, 0.9, 4, tc))
+    out = fva.fva_permute_tokens(oc, perm, fva.FVA_FROM_CURVE)
 """
 
 import ctypes
@@ -29,6 +38,9 @@ FVA_SCHED_PERSISTENT = 0
 FVA_SCHED_NAIVE = 1
 FVA_TRACE = 2
 
+FVA_TO_CURVE = 0
+FVA_FROM_CURVE = 1
+
 
 def FVA_SPLIT_BLOCKS(s: int) -> int:
     """Flag bits forcing chunks of at most s kept blocks per split row (persistent scheduler)."""
@@ -41,6 +53,9 @@ EXPORTED = (
     "fva_attn_workspace_size",
     "fva_trace_words",
     "fva_attn",
+    "fva_curve_workspace_size",
+    "fva_curve_order",
+    "fva_permute_tokens",
     "fva_status_string",
 )
 
@@ -79,6 +94,11 @@ class Tiling:
     def tokens(self) -> int:
         return self.T * self.H * self.W
 
+    @classmethod
+    def curve(cls, tokens: int, block: int) -> "Tiling":
+        """One-dimensional tiling of a curve-ordered sequence: runs of `block` tokens."""
+        return cls(1, 1, int(tokens), 1, 1, int(block))
+
 
 class FvaError(RuntimeError):
     def __init__(self, status: int, where: str):
@@ -115,6 +135,9 @@ def _load():
             ctypes.c_int,
             [P, P, P, D, T, P, P, P, ctypes.c_float, ctypes.c_uint32, P, P, ctypes.c_size_t, P, P],
         ),
+        "fva_curve_workspace_size": (ctypes.c_int, [ctypes.c_int32] * 3 + [sz]),
+        "fva_curve_order": (ctypes.c_int, [ctypes.c_int32] * 3 + [P, P, ctypes.c_size_t, P]),
+        "fva_permute_tokens": (ctypes.c_int, [P, P, D, P, ctypes.c_int32, P]),
         "fva_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     }
     for name, (res, args) in sigs.items():
@@ -236,6 +259,47 @@ def fva_attn(q, k, v, tiling: Tiling, mask, counts=None, kv_idx=None, *, scale: 
         ctypes.c_size_t(ws.numel() * ws.element_size()), _ptr(trace), _stream_ptr(torch, stream),
     )
     _check(st, "fva_attn")
+    return out
+
+
+def fva_curve_workspace_size(T: int, H: int, W: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.fva_curve_workspace_size(int(T), int(H), int(W), ctypes.byref(n)), "fva_curve_workspace_size")
+    return n.value
+
+
+def fva_curve_order(T: int, H: int, W: int, *, device=None, out=None, workspace=None, stream=None):
+    """perm[r] = raster token id of the token of Hilbert-curve rank r (int32 device tensor)."""
+    import torch
+
+    dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+    N = int(T) * int(H) * int(W)
+    perm = out if out is not None else torch.empty(N, dtype=torch.int32, device=dev)
+    if perm.dtype != torch.int32 or perm.numel() != N or not perm.is_contiguous() or not perm.is_cuda:
+        raise ValueError("perm must be a contiguous int32 device tensor of T*H*W entries")
+    ws = _workspace(torch, fva_curve_workspace_size(T, H, W), perm.device, workspace)
+    st = lib.fva_curve_order(int(T), int(H), int(W), _ptr(perm), _ptr(ws),
+                             ctypes.c_size_t(ws.numel() * ws.element_size()), _stream_ptr(torch, stream))
+    _check(st, "fva_curve_order")
+    return perm
+
+
+def fva_permute_tokens(x, perm, direction: int, *, out=None, stream=None):
+    """Token rows of x into (FVA_TO_CURVE) or out of (FVA_FROM_CURVE) curve order."""
+    import torch
+
+    if x.dtype != torch.bfloat16 or not x.is_cuda:
+        raise ValueError("x must be a bf16 device tensor")
+    if perm.dtype != torch.int32 or not perm.is_cuda or not perm.is_contiguous() or perm.numel() != x.shape[2]:
+        raise ValueError("perm must be a contiguous int32 device tensor with one entry per token")
+    desc = _desc_of(x)
+    if out is None:
+        out = torch.empty_strided(x.shape, x.stride(), dtype=torch.bfloat16, device=x.device)
+    elif out.stride() != x.stride() or out.shape != x.shape or out.dtype != torch.bfloat16:
+        raise ValueError("out must match x in shape, strides and dtype")
+    st = lib.fva_permute_tokens(_ptr(x), _ptr(out), ctypes.byref(desc), _ptr(perm), int(direction),
+                                _stream_ptr(torch, stream))
+    _check(st, "fva_permute_tokens")
     return out
 
 

@@ -167,6 +167,16 @@ __device__ __forceinline__ void row_offsets(const AttnParams& P, const BlockMap&
     const int l = lq * sn2;
 #pragma unroll
     for (int u = 0; u < 8; ++u) roff[u] = a + ((u & 3) * W + 4 * (u >> 2)) * sn2 + l;
+  } else if (m.n == m.ex) {
+    // One line of consecutive tokens (a one-dimensional block, such as a run
+    // of the Hilbert curve): key kap is token tbase + kap, clamped to the
+    // last real row.
+    const int last = m.n - 1;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int kap = min(32 * w + 8 * (u & 3) + 4 * (u >> 2) + lq, last);
+      roff[u] = (m.tbase + kap) * sn2;
+    }
   } else {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {

@@ -38,6 +38,15 @@ fva_status check_shape(const fva_qkv_desc* d, const fva_tiling* t, int* nb_out) 
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Largest grid extent of the curve order: curve indices stay below 8^8.
+constexpr int kMaxCurveExtent = 256;
+
+fva_status check_curve_grid(int32_t T, int32_t H, int32_t W) {
+  if (T <= 0 || H <= 0 || W <= 0) return FVA_ERR_SHAPE;
+  if (T > kMaxCurveExtent || H > kMaxCurveExtent || W > kMaxCurveExtent) return FVA_ERR_UNSUPPORTED;
+  return FVA_OK;
+}
+
 // Scheduling bits, the trace bit and a forced chunk size in bits 8..23.
 constexpr uint32_t kAttnFlags = 3u | (0xFFFFu << 8);
 
@@ -156,12 +165,50 @@ fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_d
   return fva::launch_attn(a) == hipSuccess ? FVA_OK : FVA_ERR_HIP;
 }
 
+fva_status fva_curve_workspace_size(int32_t T, int32_t H, int32_t W, size_t* bytes) {
+  if (!bytes) return FVA_ERR_INVALID_ARG;
+  const fva_status s = check_curve_grid(T, H, W);
+  if (s != FVA_OK) return s;
+  *bytes = fva::curve_workspace_bytes(T, H, W);
+  return FVA_OK;
+}
+
+fva_status fva_curve_order(int32_t T, int32_t H, int32_t W, int32_t* perm, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  if (!perm) return FVA_ERR_INVALID_ARG;
+  const fva_status s = check_curve_grid(T, H, W);
+  if (s != FVA_OK) return s;
+  const size_t need = fva::curve_workspace_bytes(T, H, W);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;
+  return fva::launch_curve_order(T, H, W, perm, workspace, reinterpret_cast<hipStream_t>(stream)) == hipSuccess
+             ? FVA_OK
+             : FVA_ERR_HIP;
+}
+
+fva_status fva_permute_tokens(const void* src, void* dst, const fva_qkv_desc* desc, const int32_t* perm,
+                              int32_t direction, void* stream) {
+  if (!src || !dst || !desc || !perm) return FVA_ERR_INVALID_ARG;
+  if (direction != FVA_TO_CURVE && direction != FVA_FROM_CURVE) return FVA_ERR_INVALID_ARG;
+  if (src == dst) return FVA_ERR_INVALID_ARG;
+  if (!aligned16(src) || !aligned16(dst)) return FVA_ERR_INVALID_ARG;
+  const fva_qkv_desc* d = desc;
+  if (d->batch < 0 || d->heads < 0 || d->tokens <= 0) return FVA_ERR_SHAPE;
+  if (d->head_dim != fva::kHeadDim) return FVA_ERR_UNSUPPORTED;
+  if (d->stride_n < d->head_dim || d->stride_h < 0 || d->stride_b < 0) return FVA_ERR_SHAPE;
+  if (d->stride_n % 8 != 0 || d->stride_h % 8 != 0 || d->stride_b % 8 != 0) return FVA_ERR_SHAPE;
+  if ((int64_t)d->batch * d->heads > 65535) return FVA_ERR_UNSUPPORTED;
+  return fva::launch_permute_rows(src, dst, d->batch, d->heads, d->tokens, d->stride_b, d->stride_h, d->stride_n, perm,
+                                  direction, reinterpret_cast<hipStream_t>(stream)) == hipSuccess
+             ? FVA_OK
+             : FVA_ERR_HIP;
+}
+
 const char* fva_status_string(fva_status status) {
   switch (status) {
     case FVA_OK: return "ok";
     case FVA_ERR_INVALID_ARG: return "invalid argument";
     case FVA_ERR_SHAPE: return "shape mismatch";
-    case FVA_ERR_UNSUPPORTED: return "unsupported shape (head_dim must be 128, tile volume 64 or 128, nb <= 1024)";
+    case FVA_ERR_UNSUPPORTED: return "unsupported shape (head_dim must be 128, tile volume 64 or 128, nb <= 1024, curve grid extents <= 256)";
     case FVA_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case FVA_ERR_HIP: return "HIP launch failed";
   }

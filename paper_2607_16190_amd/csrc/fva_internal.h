@@ -47,4 +47,10 @@ int64_t attn_trace_words(int batch, int heads, int nb);
 hipError_t launch_route(const RouteArgs& a);
 hipError_t launch_attn(const AttnArgs& a);
 
+// Hilbert-curve token order and row permutation (curve_kernels.hip).
+size_t curve_workspace_bytes(int T, int H, int W);
+hipError_t launch_curve_order(int T, int H, int W, int32_t* perm, void* workspace, hipStream_t stream);
+hipError_t launch_permute_rows(const void* src, void* dst, int batch, int heads, int tokens, int64_t sb, int64_t sh,
+                               int64_t sn, const int32_t* perm, int direction, hipStream_t stream);
+
 }  // namespace fva

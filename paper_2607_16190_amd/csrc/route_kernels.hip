@@ -91,8 +91,10 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
     nreal = (double)box.n;
     const int jend = (box.n + 4 * kPoolRowsPerStep - 1) / (4 * kPoolRowsPerStep) * kPoolRowsPerStep;
     // For full 8x8 planes, row r = slot + 4j sits at plane j / 16, line
-    // (j / 2) % 8, column slot + 4 (j % 2): no divisions.
+    // (j / 2) % 8, column slot + 4 (j % 2); in a one-line block it is token
+    // x0 + r: no divisions either way.
     const bool fast = box.ey == 8 && box.ex == 8;
+    const bool line = box.n == box.ex;  // consecutive tokens: row r is token x0 + r
     const int HW = g.H * g.W;
     const int tb = (box.t0 * g.H + box.y0) * g.W + box.x0 + slot;
     for (int j0 = 0; j0 < jend; j0 += kPoolRowsPerStep) {
@@ -102,7 +104,8 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
         const int j = j0 + jj;
         const int r = slot + 4 * j;
         if (r < box.n) {
-          const int tok = fast ? tb + (j >> 4) * HW + ((j >> 1) & 7) * g.W + 4 * (j & 1) : box_token(g, box, r);
+          const int tok = fast ? tb + (j >> 4) * HW + ((j >> 1) & 7) * g.W + 4 * (j & 1)
+                          : line ? tb + 4 * j : box_token(g, box, r);
           const int64_t off = base + (int64_t)tok * sn;
           vq[jj] = *reinterpret_cast<const uint4*>(Q + off);
           vk[jj] = *reinterpret_cast<const uint4*>(K + off);

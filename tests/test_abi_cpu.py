@@ -132,6 +132,51 @@ def test_attn_argument_errors():
     assert _attn(wsb=10) == fva.FVA_ERR_WORKSPACE
 
 
+def test_curve_workspace_sizes():
+    al = lambda x: (x + 255) // 256 * 256
+    # 8^k-bit bitmap and its word prefixes (max(1, 8^k / 32) words each), one index per token
+    for (T, H, W), k in (((21, 45, 80), 7), ((3, 16, 16), 4), ((1, 1, 1), 0), ((2, 2, 1), 1), ((1, 256, 3), 8)):
+        words = max(1, 8**k // 32)
+        assert fva.fva_curve_workspace_size(T, H, W) == 2 * al(words * 4) + al(T * H * W * 4)
+    for grid, status in (((0, 4, 4), fva.FVA_ERR_SHAPE), ((4, -1, 4), fva.FVA_ERR_SHAPE),
+                         ((257, 4, 4), fva.FVA_ERR_UNSUPPORTED), ((4, 4, 300), fva.FVA_ERR_UNSUPPORTED)):
+        with pytest.raises(fva.FvaError) as e:
+            fva.fva_curve_workspace_size(*grid)
+        assert e.value.status == status
+
+
+def test_curve_argument_errors():
+    L = fva.lib
+    assert L.fva_curve_order(21, 45, 80, None, FAKE, ctypes.c_size_t(1 << 30), None) == fva.FVA_ERR_INVALID_ARG
+    assert L.fva_curve_order(21, 45, 80, FAKE, None, ctypes.c_size_t(1 << 30), None) == fva.FVA_ERR_WORKSPACE
+    assert L.fva_curve_order(21, 45, 80, FAKE, FAKE, ctypes.c_size_t(1000), None) == fva.FVA_ERR_WORKSPACE
+    assert L.fva_curve_order(21, 45, 0, FAKE, FAKE, ctypes.c_size_t(1 << 30), None) == fva.FVA_ERR_SHAPE
+    assert L.fva_curve_order(300, 45, 8, FAKE, FAKE, ctypes.c_size_t(1 << 30), None) == fva.FVA_ERR_UNSUPPORTED
+    other = ctypes.c_void_p(0x7F0000100000)
+    d = desc()
+    P = lambda src=FAKE, dst=other, dd=d, perm=FAKE, direction=fva.FVA_TO_CURVE: L.fva_permute_tokens(
+        src, dst, ctypes.byref(dd) if dd is not None else None, perm, direction, None)
+    assert P(src=None) == fva.FVA_ERR_INVALID_ARG
+    assert P(perm=None) == fva.FVA_ERR_INVALID_ARG
+    assert P(dd=None) == fva.FVA_ERR_INVALID_ARG
+    assert P(dst=FAKE) == fva.FVA_ERR_INVALID_ARG  # in place
+    assert P(direction=2) == fva.FVA_ERR_INVALID_ARG
+    assert P(dst=ctypes.c_void_p(0x7F0000100008)) == fva.FVA_ERR_INVALID_ARG  # not 16-byte aligned
+    assert P(dd=desc(D=64)) == fva.FVA_ERR_UNSUPPORTED
+    assert P(dd=desc(N=0)) == fva.FVA_ERR_SHAPE
+    bad = desc()
+    bad.stride_n = 100
+    assert P(dd=bad) == fva.FVA_ERR_SHAPE
+    assert P(dd=desc(B=2, H=40000)) == fva.FVA_ERR_UNSUPPORTED  # more than 65535 heads in all
+
+
+def test_curve_tiling_block_counts():
+    assert fva.fva_num_blocks(fva.Tiling.curve(75600, 128)) == 591
+    assert fva.fva_num_blocks(fva.Tiling.curve(32760, 128)) == 256
+    assert fva.fva_num_blocks(fva.Tiling.curve(768, 64)) == 12
+    assert fva.fva_attn_workspace_size(desc(), fva.Tiling.curve(75600, 128)) > 0
+
+
 def test_status_strings():
     assert fva.fva_status_string(0) == "ok"
     for s in (-1, -2, -3, -4, -5):
