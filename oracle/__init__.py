@@ -17,7 +17,10 @@ Balancing for Video Generation"):
   importance reaches p -- §2.1;
 * Top-k safety floor -- §2.1 and §3.1;
 * realised per-head workload L_h = mean_i sum_j M_{h,i,j} -- §2.2, Eq. 1;
-* block-sparse attention over the retained blocks only -- §2.1, §3.1.
+* block-sparse attention over the retained blocks only -- §2.1, §3.1;
+* the quantised-V variant (E4M3 codec, per-channel power-of-two scales,
+  bound on the rounding of P) -- §3.4 (GPU-side V quantisation), in
+  fp8.py, imported on its own.
 
 Parity status of each function is stated in its docstring. One part is
 "parity unpinned": whether these masks equal the masks of the paper's own
