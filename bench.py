@@ -37,6 +37,10 @@ if ROOT not in sys.path:
 
 METRIC = "sparse attn ms + dense-equiv TFLOPS, MFMA util on kept blocks; route GB/s"
 PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP8_TFLOPS = 5000.0
+# Q K^T (bf16) and P V (fp8) are equal halves of the attention flops: at both
+# peaks a launch would take flops/2 / 2500 + flops/2 / 5000 TFLOP-seconds.
+PEAK_BF16_FP8_TFLOPS = 2.0 / (1.0 / PEAK_BF16_TFLOPS + 1.0 / PEAK_FP8_TFLOPS)
 PEAK_HBM_GBPS = 8000.0
 
 
@@ -241,6 +245,8 @@ def main():
     ap.add_argument("--p", type=float, default=None)
     ap.add_argument("--p-sweep", default=None, help="comma-separated p values, timed after the main run")
     ap.add_argument("--sched", choices=["persistent", "naive"], default="persistent")
+    ap.add_argument("--v", choices=["bf16", "fp8"], default="bf16", dest="vfmt",
+                    help="attention on bf16 V, or on E4M3 V quantised inside the step")
     ap.add_argument("--blocks", choices=["box", "hilbert"], default="box",
                     help="3D boxes, or runs of the Hilbert curve over curve-ordered tokens")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -299,14 +305,29 @@ def main():
     ws_a = torch.empty(fva.fva_attn_workspace_size(desc, tiling), dtype=torch.uint8, device=dev)
     flags = fva.FVA_SCHED_NAIVE if args.sched == "naive" else fva.FVA_SCHED_PERSISTENT
     stream = torch.cuda.current_stream()
+    fp8 = args.vfmt == "fp8"
+    if fp8:
+        v8 = torch.empty((B, H, nb, 128, 128), dtype=torch.uint8, device=dev)
+        vexp = torch.empty((B, H, 128), dtype=torch.int32, device=dev)
+        ws_q = torch.empty(fva.fva_quantize_v_workspace_size(desc, tiling), dtype=torch.uint8, device=dev)
+
+    def attend(fl, trace=None):
+        if fp8:
+            fva.fva_attn_fp8v(q, k, v8, vexp, tiling, mask, counts, kv, flags=fl, out=out, workspace=ws_a, trace=trace)
+        else:
+            fva.fva_attn(q, k, v, tiling, mask, counts, kv, flags=fl, out=out, workspace=ws_a, trace=trace)
 
     def step(pp, ev=None):
         if ev:
             ev[0].record(stream)
+        if fp8:
+            fva.fva_quantize_v(v, tiling, out=(v8, vexp), workspace=ws_q)
+        if ev:
+            ev[3].record(stream)
         fva.fva_route(q, k, pp, cfg.k_min, tiling, out=(mask, counts, kv), workspace=ws_r)
         if ev:
             ev[1].record(stream)
-        fva.fva_attn(q, k, v, tiling, mask, counts, kv, flags=flags, out=out, workspace=ws_a)
+        attend(flags)
         if ev:
             ev[2].record(stream)
 
@@ -314,20 +335,23 @@ def main():
         for _ in range(warmup):
             step(pp)
         torch.cuda.synchronize()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for s_ in range(steps):
             step(pp, evs[s_])
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        route_ms = [e[0].elapsed_time(e[1]) for e in evs]
+        quant_ms = [e[0].elapsed_time(e[3]) for e in evs]
+        route_ms = [e[3].elapsed_time(e[1]) for e in evs]
         attn_ms = [e[1].elapsed_time(e[2]) for e in evs]
+        timed.quant_s = float(np.mean(quant_ms)) / 1e3
         return wall * 1e3 / steps, float(np.mean(route_ms)) / 1e3, float(np.mean(attn_ms)) / 1e3
 
     ms_per_step, t_route, t_attn = timed(p, args.steps, args.warmup)
+    t_quant = timed.quant_s
     log(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step (route {t_route*1e6:.1f} us, "
-        f"attn {t_attn*1e3:.3f} ms)")
+        f"attn {t_attn*1e3:.3f} ms" + (f", V quantisation {t_quant*1e6:.1f} us)" if fp8 else ")"))
 
     m_np = mask.cpu().numpy()
     c_np = counts.cpu().numpy()
@@ -343,13 +367,14 @@ def main():
     shared = [os.path.join(csrc, f) for f in ("fva_common.h", "fva_geometry.h")]
     digest = source_digest(os.path.join(csrc, "attn_kernels.hip"), *shared)
     traffic = None
-    bench_workload = cfg.name if curve is None else cfg.name + "-hilbert"
+    bench_workload = (cfg.name if curve is None else cfg.name + "-hilbert") + ("-fp8v" if fp8 else "")
     if ATTN_TRAFFIC["source_digest"] == digest and args.sched == "persistent":
         traffic = ATTN_TRAFFIC["bytes"].get(bench_workload)
     route_digest = source_digest(os.path.join(csrc, "route_kernels.hip"), *shared)
     route_traffic = None
     if ROUTE_TRAFFIC["source_digest"] == route_digest:
         route_traffic = ROUTE_TRAFFIC["bytes"].get(bench_workload)
+    peak = PEAK_BF16_FP8_TFLOPS if fp8 else PEAK_BF16_TFLOPS
     res = {
         "metric": METRIC,
         "value": round(dense_flops / (ms_per_step / 1e3) / 1e12, 2),
@@ -361,14 +386,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16 Q/K, e4m3 V and P (fp32 accumulation)" if fp8 else "bf16",
         "data": "synthetic (seeded video-shaped Q/K/V, sinusoidal (t,y,x) embedding, per-head alpha)",
         "config": {
             "workload": f"{cfg.name}: {H} heads, d=128, latent grid {'x'.join(map(str, cfg.grid))} = {N} tokens, "
             + (f"tile {'x'.join(map(str, cfg.tile))}" if curve is None
                else f"Hilbert-curve blocks of {int(np.prod(cfg.tile))} tokens")
-            + f", nb={nb}, p={p}, k_min={cfg.k_min}",
+            + f", nb={nb}, p={p}, k_min={cfg.k_min}" + (", E4M3 V (quantised each step)" if fp8 else ""),
             "blocks": args.blocks,
+            "v": args.vfmt,
             "batch": B,
             "heads": H,
             "tokens": N,
@@ -378,6 +404,7 @@ def main():
             "parallelism": "single GPU",
         },
         "attn_ms": round(t_attn * 1e3, 4),
+        **({"v_quantise_us": round(t_quant * 1e6, 1)} if fp8 else {}),
         "route_us": round(t_route * 1e6, 2),
         "route_GBps": round(route_bytes / t_route / 1e9, 1),
         "route_frac_hbm": round(route_bytes / t_route / 1e9 / PEAK_HBM_GBPS, 4),
@@ -392,17 +419,20 @@ def main():
         },
         "kept_tile_TFLOPS": round(kept_tile_flops / t_attn / 1e12, 2),
         "kept_tile_frac_bf16_peak": round(kept_tile_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "kept_tile_frac_peak": round(kept_tile_flops / t_attn / 1e12 / peak, 4),
         "useful_TFLOPS": round(useful_flops / t_attn / 1e12, 2),
         "dense_equiv_attn_TFLOPS": round(dense_flops / t_attn / 1e12, 2),
         "retained_fraction": round(kept / (B * H * nb * nb), 4),
         "roofline": {
             "bound": "mfma",
             "achieved": round(useful_flops / t_attn / 1e12, 2),
-            "peak": PEAK_BF16_TFLOPS,
+            "peak": round(peak, 1),
             "unit": "TFLOP/s",
-            "frac": round(useful_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "frac": round(useful_flops / t_attn / 1e12 / peak, 4),
             "traffic": traffic,
-            "kernel": "attn_persistent_kernel (fva_attn; timed with its plan_kernel)",
+            "kernel": "attn_persistent_kernel (fva_attn; timed with its plan_kernel)" if not fp8 else
+            "attn_persistent_kernel<true> (fva_attn_fp8v; timed with its plan_kernel); peak = bf16 Q K^T and "
+            "fp8 P V at their own peaks",
             "algorithmic_flops_per_launch": useful_flops,
             "attn_source_digest": digest,
         },
@@ -415,8 +445,7 @@ def main():
         imb = {}
         for name, fl in (("persistent", fva.FVA_SCHED_PERSISTENT), ("naive", fva.FVA_SCHED_NAIVE)):
             trace.zero_()
-            fva.fva_attn(q, k, v, tiling, mask, counts, kv, flags=fl | fva.FVA_TRACE, out=out, workspace=ws_a,
-                         trace=trace)
+            attend(fl | fva.FVA_TRACE, trace)
             torch.cuda.synchronize()
             imb[name] = imbalance(trace.cpu().numpy(), c_np)
         res["scheduler_trace"] = imb

@@ -226,6 +226,59 @@ fva_status fva_curve_order(int32_t T, int32_t H, int32_t W, int32_t* perm, void*
 fva_status fva_permute_tokens(const void* src, void* dst, const fva_qkv_desc* desc, const int32_t* perm,
                               int32_t direction, void* stream);
 
+/*
+ * FP8 (E4M3) quantised-V attention (§3.4: V is quantised on the GPU before
+ * attention on every step; the format is not named there).
+ *
+ * Format: OCP E4M3 (bias 7, largest finite 448, subnormals m * 2^-9),
+ * round to nearest even. Every (batch, head, channel d) has a power-of-two
+ * scale 2^e_d, e_d = max(-127, min{e : amax_d * 2^-e <= 448}) with
+ * amax_d = max over the head's tokens of |V[., d]|, and the code of V[n, d]
+ * is E4M3(V[n, d] * 2^-e_d) (exact scaling, one rounding).
+ *
+ * V8 layout (one 16 KB tile per block): uint8 [batch, heads, nb, 128 d,
+ * 128 p]; byte (d, p) of block j holds channel d of the block's real key
+ * number kap(p) (keys numbered as the tiling packs them: local raster order
+ * of a box, consecutive positions of a one-dimensional block) with
+ *   p = 32 g + 16 hb + 4 t + r (g, t in 0..3; hb in 0..1; r in 0..3),
+ *   kap(p) = 64 hb + 32 (t / 2) + 8 g + 4 (t % 2) + r,
+ * and 0 where kap(p) is past the block's real keys. v_exp: int32
+ * [batch, heads, 128] = e_d.
+ */
+/* Bytes of the V8 tensor for this shape (batch*heads*nb*16384). Host only. */
+fva_status fva_v8_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes);
+
+/* Workspace bytes of fva_quantize_v: one uint32 per (batch, head, channel),
+ * 256-byte aligned. Host only. */
+fva_status fva_quantize_v_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes);
+
+/*
+ * fva_quantize_v -- V (bf16, desc's layout) to V8 and v_exp as above; both
+ * outputs fully written (V8 16-byte aligned, v_exp 4-byte aligned).
+ * Deterministic: the codes are the format's rounding, bit for bit.
+ * Errors as for fva_route (shape, alignment, workspace), and
+ * FVA_ERR_UNSUPPORTED for batch*heads > 65535.
+ */
+fva_status fva_quantize_v(const void* V, const fva_qkv_desc* desc, const fva_tiling* tiling, uint8_t* V8,
+                          int32_t* v_exp, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * fva_attn_fp8v -- fva_attn with V replaced by its E4M3 quantisation (V8,
+ * v_exp from fva_quantize_v with the same desc and tiling). Q K^T and the
+ * online softmax are as in fva_attn; the probabilities of each kept block
+ * are rounded to E4M3 (as P * 2^7, relative error <= 2^-4 in the format's
+ * normal range, values below about 2^-17 of the row's running maximum
+ * flush to zero) and multiplied with V8 on the fp8 matrix unit (fp32
+ * accumulation), the V and P scales entering as the MFMA's power-of-two
+ * block scales. The softmax denominator is the sum of the same rounded
+ * probabilities. Flags, counts/kv_idx, workspace (fva_attn_workspace_size),
+ * trace and O are as for fva_attn.
+ */
+fva_status fva_attn_fp8v(const void* Q, const void* K, const uint8_t* V8, const int32_t* v_exp,
+                         const fva_qkv_desc* desc, const fva_tiling* tiling, const uint8_t* block_mask,
+                         const int32_t* counts, const int32_t* kv_idx, float softmax_scale, uint32_t flags, void* O,
+                         void* workspace, size_t workspace_bytes, void* trace, void* stream);
+
 /* Static description of a status code. */
 const char* fva_status_string(fva_status status);
 

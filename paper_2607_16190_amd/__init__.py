@@ -56,6 +56,10 @@ EXPORTED = (
     "fva_curve_workspace_size",
     "fva_curve_order",
     "fva_permute_tokens",
+    "fva_v8_size",
+    "fva_quantize_v_workspace_size",
+    "fva_quantize_v",
+    "fva_attn_fp8v",
     "fva_status_string",
 )
 
@@ -138,6 +142,13 @@ def _load():
         "fva_curve_workspace_size": (ctypes.c_int, [ctypes.c_int32] * 3 + [sz]),
         "fva_curve_order": (ctypes.c_int, [ctypes.c_int32] * 3 + [P, P, ctypes.c_size_t, P]),
         "fva_permute_tokens": (ctypes.c_int, [P, P, D, P, ctypes.c_int32, P]),
+        "fva_v8_size": (ctypes.c_int, [D, T, sz]),
+        "fva_quantize_v_workspace_size": (ctypes.c_int, [D, T, sz]),
+        "fva_quantize_v": (ctypes.c_int, [P, D, T, P, P, P, ctypes.c_size_t, P]),
+        "fva_attn_fp8v": (
+            ctypes.c_int,
+            [P, P, P, P, D, T, P, P, P, ctypes.c_float, ctypes.c_uint32, P, P, ctypes.c_size_t, P, P],
+        ),
         "fva_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     }
     for name, (res, args) in sigs.items():
@@ -300,6 +311,73 @@ def fva_permute_tokens(x, perm, direction: int, *, out=None, stream=None):
     st = lib.fva_permute_tokens(_ptr(x), _ptr(out), ctypes.byref(desc), _ptr(perm), int(direction),
                                 _stream_ptr(torch, stream))
     _check(st, "fva_permute_tokens")
+    return out
+
+
+def fva_v8_size(desc: _Desc, tiling: Tiling) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.fva_v8_size(ctypes.byref(desc), ctypes.byref(tiling.c()), ctypes.byref(n)), "fva_v8_size")
+    return n.value
+
+
+def fva_quantize_v_workspace_size(desc: _Desc, tiling: Tiling) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.fva_quantize_v_workspace_size(ctypes.byref(desc), ctypes.byref(tiling.c()), ctypes.byref(n)),
+           "fva_quantize_v_workspace_size")
+    return n.value
+
+
+def fva_quantize_v(v, tiling: Tiling, *, out=None, workspace=None, stream=None):
+    """E4M3 tiles and per-channel exponents of V (see include/fva.h). Returns (v8, v_exp)."""
+    import torch
+
+    if v.dtype != torch.bfloat16 or not v.is_cuda:
+        raise ValueError("v must be a bf16 device tensor")
+    desc = _desc_of(v)
+    nb = fva_num_blocks(tiling)
+    B, H = v.shape[0], v.shape[1]
+    if out is None:
+        v8 = torch.empty((B, H, max(nb, 0), 128, 128), dtype=torch.uint8, device=v.device)
+        vexp = torch.empty((B, H, 128), dtype=torch.int32, device=v.device)
+    else:
+        v8, vexp = out
+    if v8.numel() < fva_v8_size(desc, tiling) or not v8.is_contiguous() or vexp.numel() < B * H * 128:
+        raise ValueError("v8 / v_exp too small or not contiguous")
+    ws = _workspace(torch, fva_quantize_v_workspace_size(desc, tiling), v.device, workspace)
+    st = lib.fva_quantize_v(_ptr(v), ctypes.byref(desc), ctypes.byref(tiling.c()), _ptr(v8), _ptr(vexp), _ptr(ws),
+                            ctypes.c_size_t(ws.numel() * ws.element_size()), _stream_ptr(torch, stream))
+    _check(st, "fva_quantize_v")
+    return v8, vexp
+
+
+def fva_attn_fp8v(q, k, v8, vexp, tiling: Tiling, mask, counts=None, kv_idx=None, *, scale: float = 0.0,
+                  flags: int = 0, out=None, workspace=None, trace=None, stream=None):
+    """Block-sparse attention with E4M3 V (see include/fva.h). Returns O (bf16, q's layout)."""
+    import torch
+
+    for t in (q, k):
+        if t.dtype != torch.bfloat16 or not t.is_cuda:
+            raise ValueError("q, k must be bf16 device tensors")
+    if q.shape != k.shape or q.stride() != k.stride():
+        raise ValueError("q and k must share shape and strides")
+    if v8.dtype != torch.uint8 or vexp.dtype != torch.int32 or not v8.is_contiguous() or not vexp.is_contiguous():
+        raise ValueError("v8 must be contiguous uint8 and v_exp contiguous int32 (from fva_quantize_v)")
+    desc = _desc_of(q)
+    if v8.numel() < fva_v8_size(desc, tiling) or vexp.numel() < q.shape[0] * q.shape[1] * 128:
+        raise ValueError("v8 / v_exp do not match q and the tiling")
+    if out is None:
+        out = torch.empty_strided(q.shape, q.stride(), dtype=torch.bfloat16, device=q.device)
+    elif out.stride() != q.stride() or out.shape != q.shape or out.dtype != torch.bfloat16:
+        raise ValueError("out must match q in shape, strides and dtype")
+    ws = _workspace(torch, fva_attn_workspace_size(desc, tiling, flags), q.device, workspace)
+    if (flags & FVA_TRACE) and trace is None:
+        raise ValueError("FVA_TRACE needs a trace tensor of fva_trace_words int64")
+    st = lib.fva_attn_fp8v(
+        _ptr(q), _ptr(k), _ptr(v8), _ptr(vexp), ctypes.byref(desc), ctypes.byref(tiling.c()), _ptr(mask),
+        _ptr(counts), _ptr(kv_idx), ctypes.c_float(scale), int(flags), _ptr(out), _ptr(ws),
+        ctypes.c_size_t(ws.numel() * ws.element_size()), _ptr(trace), _stream_ptr(torch, stream),
+    )
+    _check(st, "fva_attn_fp8v")
     return out
 
 

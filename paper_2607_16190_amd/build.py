@@ -9,7 +9,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libfva.so")
 
-SOURCES = ["fva_abi.cpp", "route_kernels.hip", "attn_kernels.hip", "curve_kernels.hip"]
+SOURCES = ["fva_abi.cpp", "route_kernels.hip", "attn_kernels.hip", "curve_kernels.hip", "fp8_kernels.hip"]
 HEADERS = ["fva_common.h", "fva_geometry.h", "fva_internal.h"]
 
 FLAGS = [

@@ -41,6 +41,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kAttnThreads = 256;
 constexpr int kRowBytes = 256;                 // one 128-dim bf16 row
@@ -56,6 +58,8 @@ struct AttnParams {
   const uint16_t* Q;
   const uint16_t* K;
   const uint16_t* V;
+  const unsigned char* V8;  // E4M3 V tiles (FP8 variant)
+  const int32_t* vexp;      // their per-channel exponents
   uint16_t* O;
   int heads;
   int64_t sb, sh, sn;
@@ -216,6 +220,31 @@ __device__ __forceinline__ void issue_tile(const uint16_t* __restrict__ src, con
   }
 }
 
+// FP8 variant: asynchronous copy of this wave's 4 KB of block j's E4M3 V^T
+// tile (rows = channels, 128 bytes of key positions each). Instruction u of
+// wave w fills rows 8(4w + u) .. +7; lane L takes row L / 8 of them and the
+// 16-byte chunk at physical position L % 8, which holds logical chunk
+// (L % 8) ^ (row % 8): the reads of 16 consecutive channels at one key chunk
+// then spread over all banks.
+__device__ __forceinline__ void issue_v8_tile(const unsigned char* __restrict__ head, int j, unsigned char* tile) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int rr = lane >> 3;
+  const uint32_t lane_off = (uint32_t)(rr * 128 + 16 * ((lane & 7) ^ rr));
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)tile;
+  const uint32_t tile_off = (uint32_t)j * (uint32_t)kV8TileBytes;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int slab = 4 * w + u;
+    const uint32_t off = tile_off + (uint32_t)(slab * 1024) + lane_off;
+    const uint32_t dst = lds0 + (uint32_t)(slab * 1024);
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(dst), "v"(off), "s"(head)
+                 : "memory");
+  }
+}
+
 __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 a, f32x4 b) {
   const f32x8 v = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
   return __builtin_convertvector(v, bf16x8);
@@ -258,6 +287,12 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // kept-list entries [begin, end) of its row. partial == nullptr: the whole
 // row, normalised into O; otherwise one chunk of a split row, whose
 // unnormalised result goes to partial for the combine step.
+//
+// F8 (the quantised-V variant): V comes as E4M3 tiles with per-channel
+// power-of-two scales; the probabilities of a whole block are rounded to
+// E4M3 and multiplied with one 16x16x128 fp8 MFMA per (channel tile, query
+// tile), the scales entering as the MFMA's E8M0 block scales.
+template <bool F8>
 __device__ void process_item(const AttnParams& P, int row, int begin, int end, float* __restrict__ partial,
                              unsigned char* __restrict__ Ks, unsigned char* __restrict__ Vs) {
   const int nb = P.g.nb;
@@ -277,6 +312,22 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   const int l16 = lane & 15;
   const int row0 = wave * 32;
   const bool active = row0 < bi.n;
+
+  // FP8 variant: the head's E4M3 V tiles, and the E8M0 scale 127 + e_d of
+  // each of the lane's channels d = 16mt + l16, one byte each, four per
+  // register (extracted per use: the MFMA takes a scale register whose
+  // upper bytes are zero).
+  const unsigned char* V8h = nullptr;
+  int scv[2] = {0, 0};
+  if constexpr (F8) {
+    V8h = P.V8 + (int64_t)bh * nb * kV8TileBytes;
+    const int32_t* ve = P.vexp + (int64_t)bh * 128 + l16;
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) {
+      const int sc = min(max(127 + ve[16 * mt], 0), 254);
+      scv[mt >> 2] |= sc << (8 * (mt & 3));
+    }
+  }
 
   // counts and kv_idx are read through the scalar cache (constant address
   // space: the kernel never writes them). They come from the caller: clamp
@@ -342,8 +393,9 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
     row_offsets(P, mc, roff);
     if (wave < ngroups_of(mc.n)) {
       issue_tile<false>(Kh, roff, Ks);
-      issue_tile<true>(Vh, roff, Vs);
+      if constexpr (!F8) issue_tile<true>(Vh, roff, Vs);
     }
+    if constexpr (F8) issue_v8_tile(V8h, jc, Vs);
   }
 
   auto vfrag = [&](int kg, int mt) {
@@ -482,6 +534,173 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
     __builtin_amdgcn_s_setprio(0);
   };
 
+  // ---- FP8 variant ------------------------------------------------------
+  // E4M3 V^T fragment of channel tile mt: lane (g4, l16) holds channel
+  // 16mt + l16, key positions 32g4 .. 32g4 + 31 (two 16-byte chunks, stored
+  // at physical chunk (logical ^ (channel % 8))).
+  const int v8o0 = l16 * 128 + 16 * ((2 * g4) ^ (l16 & 7));
+  const int v8o1 = l16 * 128 + 16 * ((2 * g4 + 1) ^ (l16 & 7));
+  auto v8frag = [&](int mt) {
+    const i32x4 lo = *reinterpret_cast<const i32x4*>(Vs + mt * 2048 + v8o0);
+    const i32x4 hi = *reinterpret_cast<const i32x4*>(Vs + mt * 2048 + v8o1);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  // O^T += V^T P^T over the whole block, one 16x16x128 fp8 MFMA per (channel
+  // tile, query tile). A scale: 127 + e_d, the channel's V exponent; B
+  // scale: 2^-7 (P was rounded as P * 2^7), times 2^-kb on the first half's
+  // keys when the second half moved the row's reference (sbv). The sum of P
+  // comes from the same MFMA against E4M3 ones.
+  //
+  // K order of the instruction: lane group g holds K = 16g .. 16g + 15 in its
+  // bytes 0..15 and K = 64 + 16g .. in its bytes 16..31, and the E8M0 scale of
+  // K block b (K = 32b .. 32b + 31) is lane group b's. Bytes 0..15 of every
+  // group are the first half's keys (words 0..3), so the first half is K
+  // blocks 0 and 1 (scales of lane groups 0 and 1), the second half K blocks
+  // 2 and 3.
+  auto pv_f8 = [&](const i32x8 (&p8)[2], const int (&sbv)[2]) {
+    constexpr int kPre = 2;
+    i32x8 vq[kPre + 1];
+#pragma unroll
+    for (int u = 0; u < kPre; ++u) vq[u] = v8frag(u);
+    __builtin_amdgcn_s_setprio(1);
+    auto step = [&](auto mt_c) {
+      constexpr int mt = decltype(mt_c)::value;
+      if constexpr (mt + kPre < 8) vq[(mt + kPre) % (kPre + 1)] = v8frag(mt + kPre);
+      const i32x8 va = vq[mt % (kPre + 1)];
+      const int sa = (scv[mt >> 2] >> (8 * (mt & 3))) & 0xFF;
+      o[mt][0] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(va, p8[0], o[mt][0], 0, 0, 0, sa, 0, sbv[0]);
+      o[mt][1] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(va, p8[1], o[mt][1], 0, 0, 0, sa, 0, sbv[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    static_for<0, 8>(step);
+    const i32x8 ones8 = {0x38383838, 0x38383838, 0x38383838, 0x38383838,
+                         0x38383838, 0x38383838, 0x38383838, 0x38383838};
+    lsum[0] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ones8, p8[0], lsum[0], 0, 0, 0, 127, 0, sbv[0]);
+    lsum[1] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ones8, p8[1], lsum[1], 0, 0, 0, 127, 0, sbv[1]);
+    __builtin_amdgcn_s_setprio(0);
+  };
+  // Online softmax of one half into E4M3: accumulator (t, r) of lane group
+  // g4 becomes byte r of word 4hb + t of the B operand (the order of the
+  // E4M3 V tiles). The reference moves when a row's max
+  // passes it by more than 1 (exp2 units), so P * 2^7 <= 2^8 stays inside the
+  // format (largest finite 448) and the smallest nonzero E4M3 value sits
+  // 2^-16 .. 2^-17 below the row's largest P. In the first half the move is
+  // free; in the second it is a whole number kb of powers of two, so the
+  // first half (already rounded against the old reference) is rescaled
+  // exactly through its K blocks' MFMA scale, and O and the sum of P by 2^-kb.
+  auto softmax_f8 = [&](int hb, bool short_half, int nj, f32x4 (&s)[4][2], i32x8 (&p8)[2], int (&kb)[2]) {
+    if (nj < 64 * hb + 64) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kap = 64 * hb + 32 * (t >> 1) + 8 * g4 + 4 * (t & 1) + r;
+          if (kap >= nj) {
+            s[t][0][r] = -INFINITY;
+            s[t][1][r] = -INFINITY;
+          }
+        }
+      }
+    }
+    float mx[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        mx[0] = fmaxf(mx[0], s[t][0][r]);
+        mx[1] = fmaxf(mx[1], s[t][1][r]);
+      }
+    }
+    const bool want0 = (mx[0] - mrow[0]) * P.c2 > 1.0f;
+    const bool want1 = (mx[1] - mrow[1]) * P.c2 > 1.0f;
+    if (__ballot(want0 || want1)) {
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        const float rmx = row_max4(mx[nt]);
+        const float dist = (rmx - mrow[nt]) * P.c2;
+        const bool grow = dist > 1.0f;
+        float alpha = 1.0f;
+        if (hb == 0) {
+          const float mref = grow ? rmx : mrow[nt];
+          alpha = grow ? __builtin_amdgcn_exp2f((mrow[nt] - mref) * P.c2) : 1.0f;
+          mrow[nt] = mref;
+        } else if (grow) {
+          const int k = (int)ceilf(dist - 1.0f);  // >= 1
+          kb[nt] = k;
+          mrow[nt] += (float)k / P.c2;
+          alpha = k > 126 ? 0.0f : __uint_as_float((uint32_t)(127 - k) << 23);
+        }
+        if (__ballot(grow)) {
+#pragma unroll
+          for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha;
+          lsum[nt] *= alpha;
+        }
+      }
+    }
+    const float negm[2] = {7.0f - mrow[0] * P.c2, 7.0f - mrow[1] * P.c2};
+    auto tile = [&](auto t_c) {
+      constexpr int t = decltype(t_c)::value;
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        float e[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) e[r] = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
+        int w = __builtin_amdgcn_cvt_pk_fp8_f32(e[0], e[1], 0, false);
+        w = __builtin_amdgcn_cvt_pk_fp8_f32(e[2], e[3], w, true);
+        p8[nt][4 * hb + t] = w;
+      }
+    };
+    static_for<0, 2>(tile);
+    if (!short_half) static_for<2, 4>(tile);
+  };
+  if constexpr (F8) {
+    for (int c = 0; c < cnt; ++c) {
+      const int nj = mc.n;
+      const int ng = ngroups_of(nj);
+      // K_c landed (the four copies of V8_c, issued after it, may be in flight).
+      wait_vmem<4>();
+      tile_barrier();
+      i32x8 p8[2] = {i32x8{0, 0, 0, 0, 0, 0, 0, 0}, i32x8{0, 0, 0, 0, 0, 0, 0, 0}};
+      int kb[2] = {0, 0};
+      BlockMap mn;
+      int j2 = 0;
+      {
+        f32x4 s[4][2];
+        if (active) s_phase(0, false, s);
+        // record of block c + 1 and the id of block c + 2 (clamped to the list)
+        mn = load_block_map(P.bmap, j1);
+        j2 = min(max(kvl[min(c + 2, cnt - 1)], 0), nb - 1);
+        if (active) softmax_f8(0, false, nj, s, p8, kb);
+      }
+      {
+        const bool run = ng > 2;
+        const bool short_half = ng == 3;
+        f32x4 s[4][2];
+        if (active && run) s_phase(1, short_half, s);
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the prefetched scalars
+        wait_vmem<0>();                        // V8_c landed
+        tile_barrier();                        // every wave is done with K_c and sees V8_c
+        if (c + 1 < cnt) {
+          mc = mn;
+          if (wave < ngroups_of(mc.n)) {
+            row_offsets(P, mc, roff);
+            issue_tile<false>(Kh, roff, Ks);
+          }
+        }
+        if (active && run) softmax_f8(1, short_half, nj, s, p8, kb);
+      }
+      if (active) {
+        // B scale of the K block whose scale this lane supplies: lane groups
+        // 0 and 1 scale the first half's keys, which carry the second half's
+        // reference move
+        const int sbv[2] = {g4 >= 2 ? 120 : max(120 - kb[0], 0), g4 >= 2 ? 120 : max(120 - kb[1], 0)};
+        pv_f8(p8, sbv);
+      }
+      tile_barrier();  // every wave is done with V8_c
+      if (c + 1 < cnt) issue_v8_tile(V8h, j1, Vs);
+      j1 = j2;
+    }
+  } else {
   for (int c = 0; c < cnt; ++c) {
     const int nj = mc.n;
     const int ng = ngroups_of(nj);
@@ -533,6 +752,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
     if (c + 1 < cnt && wave < ng_next) issue_tile<true>(Vh, roff, Vs);
     j1 = j2;
   }
+  }
 
   // Epilogue: O^T accumulator (mt, r) of lane (g4, l16) is head dim
   // 16mt + 4g4 + r of query row 16nt + l16.
@@ -581,11 +801,12 @@ __device__ __forceinline__ void trace_item(const AttnParams& P, int64_t rec, int
   }
 }
 
+template <bool F8>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams P) {
   __shared__ __align__(16) unsigned char ks_tile[kTileBytes];
-  __shared__ __align__(16) unsigned char vs_tile[kTileBytes];
+  __shared__ __align__(16) unsigned char vs_tile[F8 ? kV8TileBytes : kTileBytes];
   const int64_t t0 = (int64_t)wall_clock64();
-  process_item(P, blockIdx.x, 0, P.g.nb, nullptr, ks_tile, vs_tile);
+  process_item<F8>(P, blockIdx.x, 0, P.g.nb, nullptr, ks_tile, vs_tile);
   if (P.trace) {
     __syncthreads();
     trace_item(P, blockIdx.x, t0);
@@ -603,11 +824,12 @@ __device__ __forceinline__ int xcc_id() {
   return (int)(xcc & 0xfu);
 }
 
+template <bool F8>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnParams P, const int32_t* __restrict__ items,
                                                                           const int32_t* __restrict__ qbase,
                                                                           int32_t* __restrict__ qctr) {
   __shared__ __align__(16) unsigned char ks_tile[kTileBytes];
-  __shared__ __align__(16) unsigned char vs_tile[kTileBytes];
+  __shared__ __align__(16) unsigned char vs_tile[F8 ? kV8TileBytes : kTileBytes];
   __shared__ int next_slot, next_q;
   int q = xcc_id() % kQueues;
   for (;;) {
@@ -635,13 +857,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
     const int64_t t0 = (int64_t)wall_clock64();
     int64_t rec;
     if (item >= 0) {
-      process_item(P, item, 0, P.g.nb, nullptr, ks_tile, vs_tile);
+      process_item<F8>(P, item, 0, P.g.nb, nullptr, ks_tile, vs_tile);
       rec = item;
     } else {
       const int c = -1 - item;
       typedef __attribute__((address_space(4))) const int32_t const_i32;
       const const_i32* ch = (const const_i32*)(P.chunks + c);
-      process_item(P, ch[0], ch[1], ch[2], P.partials + (int64_t)c * kPartialFloats, ks_tile, vs_tile);
+      process_item<F8>(P, ch[0], ch[1], ch[2], P.partials + (int64_t)c * kPartialFloats, ks_tile, vs_tile);
       rec = c < P.trace_chunks ? P.n_rows + c : -1;
     }
     __syncthreads();  // the next item's copies overwrite the tiles; next_slot is rewritten
@@ -956,7 +1178,8 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint8_t* __restrict_
 
 struct DeviceInfo {
   int cus = 0;
-  int per_cu = 0;
+  int per_cu = 0;    // resident workgroups of the bf16 kernel per CU
+  int per_cu8 = 0;   // same for the FP8 variant
 };
 
 hipError_t device_info(DeviceInfo& info) {
@@ -969,10 +1192,14 @@ hipError_t device_info(DeviceInfo& info) {
     DeviceInfo d;
     e = hipDeviceGetAttribute(&d.cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&d.per_cu, reinterpret_cast<const void*>(&attn_persistent_kernel),
-                                                     kAttnThreads, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &d.per_cu, reinterpret_cast<const void*>(&attn_persistent_kernel<false>), kAttnThreads, 0);
+    if (e != hipSuccess) return e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &d.per_cu8, reinterpret_cast<const void*>(&attn_persistent_kernel<true>), kAttnThreads, 0);
     if (e != hipSuccess) return e;
     if (d.per_cu < 1) d.per_cu = 1;
+    if (d.per_cu8 < 1) d.per_cu8 = 1;
     cache[dev] = d;
   }
   info = cache[dev];
@@ -1085,6 +1312,9 @@ hipError_t launch_attn(const AttnArgs& a) {
   P.Q = reinterpret_cast<const uint16_t*>(a.Q);
   P.K = reinterpret_cast<const uint16_t*>(a.K);
   P.V = reinterpret_cast<const uint16_t*>(a.V);
+  P.V8 = a.V8;
+  P.vexp = a.vexp;
+  const bool f8 = a.V8 != nullptr;
   P.O = reinterpret_cast<uint16_t*>(a.O);
   P.heads = a.heads;
   P.sb = a.stride_b;
@@ -1106,7 +1336,10 @@ hipError_t launch_attn(const AttnArgs& a) {
   if (e != hipSuccess) return e;
 
   if (a.flags & 1u) {
-    hipLaunchKernelGGL(attn_naive_kernel, dim3(n_items), dim3(kAttnThreads), 0, a.stream, P);
+    if (f8)
+      hipLaunchKernelGGL(attn_naive_kernel<true>, dim3(n_items), dim3(kAttnThreads), 0, a.stream, P);
+    else
+      hipLaunchKernelGGL(attn_naive_kernel<false>, dim3(n_items), dim3(kAttnThreads), 0, a.stream, P);
     return hipGetLastError();
   }
   const int forced = (int)((a.flags >> 8) & 0xFFFFu);
@@ -1114,10 +1347,14 @@ hipError_t launch_attn(const AttnArgs& a) {
                      ws.cap, ws.items, ws.qbase, ws.qctr, ws.hscratch, ws.rscratch, ws.chunks, ws.splits, ws.n_split);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  int grid = info.cus * info.per_cu;
+  int grid = info.cus * (f8 ? info.per_cu8 : info.per_cu);
   if (grid > n_items + ws.cap) grid = n_items + ws.cap;
-  hipLaunchKernelGGL(attn_persistent_kernel, dim3(grid), dim3(kAttnThreads), 0, a.stream, P, ws.items, ws.qbase,
-                     ws.qctr);
+  if (f8)
+    hipLaunchKernelGGL(attn_persistent_kernel<true>, dim3(grid), dim3(kAttnThreads), 0, a.stream, P, ws.items,
+                       ws.qbase, ws.qctr);
+  else
+    hipLaunchKernelGGL(attn_persistent_kernel<false>, dim3(grid), dim3(kAttnThreads), 0, a.stream, P, ws.items,
+                       ws.qbase, ws.qctr);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // Split rows (if any) are merged; the workgroups beyond their number exit.

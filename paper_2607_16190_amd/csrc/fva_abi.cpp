@@ -122,10 +122,19 @@ fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, dou
   return fva::launch_route(a) == hipSuccess ? FVA_OK : FVA_ERR_HIP;
 }
 
-fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_desc* desc, const fva_tiling* tiling,
-                    const uint8_t* block_mask, const int32_t* counts, const int32_t* kv_idx, float softmax_scale,
-                    uint32_t flags, void* O, void* workspace, size_t workspace_bytes, void* trace, void* stream) {
-  if (!Q || !K || !V || !O) return FVA_ERR_INVALID_ARG;
+}  // extern "C"
+
+namespace {
+
+// fva_attn and fva_attn_fp8v: V is bf16 rows, or (V8 != null) E4M3 tiles with
+// their exponents.
+fva_status attn_common(const void* Q, const void* K, const void* V, const uint8_t* V8, const int32_t* v_exp,
+                       const fva_qkv_desc* desc, const fva_tiling* tiling, const uint8_t* block_mask,
+                       const int32_t* counts, const int32_t* kv_idx, float softmax_scale, uint32_t flags, void* O,
+                       void* workspace, size_t workspace_bytes, void* trace, void* stream) {
+  if (!Q || !K || !O) return FVA_ERR_INVALID_ARG;
+  if (!V && !V8) return FVA_ERR_INVALID_ARG;
+  if (V8 && (!v_exp || (reinterpret_cast<uintptr_t>(v_exp) & 3u))) return FVA_ERR_INVALID_ARG;
   if (flags & ~kAttnFlags) return FVA_ERR_INVALID_ARG;
   if ((counts == nullptr) != (kv_idx == nullptr)) return FVA_ERR_INVALID_ARG;
   if (!counts && !block_mask) return FVA_ERR_INVALID_ARG;
@@ -134,13 +143,17 @@ fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_d
   int nb = 0;
   const fva_status s = check_shape(desc, tiling, &nb);
   if (s != FVA_OK) return s;
-  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return FVA_ERR_INVALID_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(O)) return FVA_ERR_INVALID_ARG;
+  if (V && !aligned16(V)) return FVA_ERR_INVALID_ARG;
+  if (V8 && !aligned16(V8)) return FVA_ERR_INVALID_ARG;
   const size_t need = fva::attn_workspace_bytes(desc->batch, desc->heads, nb, flags);
   if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;
   fva::AttnArgs a;
   a.Q = Q;
   a.K = K;
   a.V = V;
+  a.V8 = V8;
+  a.vexp = v_exp;
   a.O = O;
   a.batch = desc->batch;
   a.heads = desc->heads;
@@ -163,6 +176,76 @@ fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_d
   a.workspace = workspace;
   a.stream = reinterpret_cast<hipStream_t>(stream);
   return fva::launch_attn(a) == hipSuccess ? FVA_OK : FVA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_desc* desc, const fva_tiling* tiling,
+                    const uint8_t* block_mask, const int32_t* counts, const int32_t* kv_idx, float softmax_scale,
+                    uint32_t flags, void* O, void* workspace, size_t workspace_bytes, void* trace, void* stream) {
+  if (!V) return FVA_ERR_INVALID_ARG;
+  return attn_common(Q, K, V, nullptr, nullptr, desc, tiling, block_mask, counts, kv_idx, softmax_scale, flags, O,
+                     workspace, workspace_bytes, trace, stream);
+}
+
+fva_status fva_v8_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes) {
+  if (!bytes) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  *bytes = (size_t)desc->batch * desc->heads * nb * fva::kV8TileBytes;
+  return FVA_OK;
+}
+
+fva_status fva_quantize_v_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes) {
+  if (!bytes) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  *bytes = fva::quantize_v_workspace_bytes(desc->batch, desc->heads);
+  return FVA_OK;
+}
+
+fva_status fva_quantize_v(const void* V, const fva_qkv_desc* desc, const fva_tiling* tiling, uint8_t* V8,
+                          int32_t* v_exp, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!V || !V8 || !v_exp) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  if (!aligned16(V) || !aligned16(V8) || (reinterpret_cast<uintptr_t>(v_exp) & 3u)) return FVA_ERR_INVALID_ARG;
+  if ((int64_t)desc->batch * desc->heads > 65535) return FVA_ERR_UNSUPPORTED;
+  const size_t need = fva::quantize_v_workspace_bytes(desc->batch, desc->heads);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;
+  fva::QuantizeArgs a;
+  a.V = V;
+  a.batch = desc->batch;
+  a.heads = desc->heads;
+  a.tokens = desc->tokens;
+  a.stride_b = desc->stride_b;
+  a.stride_h = desc->stride_h;
+  a.stride_n = desc->stride_n;
+  a.T = tiling->T;
+  a.H = tiling->H;
+  a.W = tiling->W;
+  a.bt = tiling->bt;
+  a.bh = tiling->bh;
+  a.bw = tiling->bw;
+  a.V8 = V8;
+  a.vexp = v_exp;
+  a.workspace = workspace;
+  a.stream = reinterpret_cast<hipStream_t>(stream);
+  return fva::launch_quantize_v(a) == hipSuccess ? FVA_OK : FVA_ERR_HIP;
+}
+
+fva_status fva_attn_fp8v(const void* Q, const void* K, const uint8_t* V8, const int32_t* v_exp,
+                         const fva_qkv_desc* desc, const fva_tiling* tiling, const uint8_t* block_mask,
+                         const int32_t* counts, const int32_t* kv_idx, float softmax_scale, uint32_t flags, void* O,
+                         void* workspace, size_t workspace_bytes, void* trace, void* stream) {
+  if (!V8 || !v_exp) return FVA_ERR_INVALID_ARG;
+  return attn_common(Q, K, nullptr, V8, v_exp, desc, tiling, block_mask, counts, kv_idx, softmax_scale, flags, O,
+                     workspace, workspace_bytes, trace, stream);
 }
 
 fva_status fva_curve_workspace_size(int32_t T, int32_t H, int32_t W, size_t* bytes) {

@@ -15,6 +15,7 @@ namespace fva {
 constexpr int kHeadDim = 128;
 constexpr int kMaxBlocks = 1024;
 constexpr int kMaxTile = 128;
+constexpr int kV8TileBytes = 128 * 128;  // one block of E4M3 V^T: 128 channels x 128 key positions
 
 struct Geometry {
   int T, H, W;

@@ -30,6 +30,8 @@ struct AttnArgs {
   int batch, heads, tokens;
   int64_t stride_b, stride_h, stride_n;
   int T, H, W, bt, bh, bw;
+  const uint8_t* V8;      // E4M3 V tiles (FP8 variant) or null
+  const int32_t* vexp;    // per-channel exponents of V8 (FP8 variant)
   const uint8_t* mask;
   const int32_t* counts;  // null: rebuilt from mask in the workspace
   const int32_t* kv_idx;  // null together with counts
@@ -40,12 +42,27 @@ struct AttnArgs {
   hipStream_t stream;
 };
 
+struct QuantizeArgs {
+  const void* V;
+  int batch, heads, tokens;
+  int64_t stride_b, stride_h, stride_n;
+  int T, H, W, bt, bh, bw;
+  uint8_t* V8;
+  int32_t* vexp;
+  void* workspace;
+  hipStream_t stream;
+};
+
 size_t route_workspace_bytes(int batch, int heads, int nb);
 size_t attn_workspace_bytes(int batch, int heads, int nb, uint32_t flags);
 int64_t attn_trace_words(int batch, int heads, int nb);
 
 hipError_t launch_route(const RouteArgs& a);
 hipError_t launch_attn(const AttnArgs& a);
+
+// E4M3 V quantisation for the FP8 attention variant (fp8_kernels.hip).
+size_t quantize_v_workspace_bytes(int batch, int heads);
+hipError_t launch_quantize_v(const QuantizeArgs& a);
 
 // Hilbert-curve token order and row permutation (curve_kernels.hip).
 size_t curve_workspace_bytes(int T, int H, int W);

@@ -23,7 +23,7 @@ FAKE = ctypes.c_void_p(0x7F0000001000)  # 4 KiB aligned, never dereferenced
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(fva_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(fva_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_every_declared_symbol_is_exported():
@@ -175,6 +175,34 @@ def test_curve_tiling_block_counts():
     assert fva.fva_num_blocks(fva.Tiling.curve(32760, 128)) == 256
     assert fva.fva_num_blocks(fva.Tiling.curve(768, 64)) == 12
     assert fva.fva_attn_workspace_size(desc(), fva.Tiling.curve(75600, 128)) > 0
+
+
+def test_fp8_sizes_and_argument_errors():
+    d = desc()
+    assert fva.fva_v8_size(d, T720) == 40 * 660 * 16384
+    assert fva.fva_quantize_v_workspace_size(d, T720) == 40 * 128 * 4
+    assert fva.fva_quantize_v_workspace_size(desc(H=3), T720) == 1536  # 3 * 128 * 4 rounded up to 256
+    L = fva.lib
+    Q = lambda v=FAKE, v8=FAKE, e=FAKE, ws=FAKE, wsb=1 << 30, dd=None: L.fva_quantize_v(
+        v, ctypes.byref(dd or d), ctypes.byref(T720.c()), v8, e, ws, ctypes.c_size_t(wsb), None)
+    assert Q(v=None) == fva.FVA_ERR_INVALID_ARG
+    assert Q(v8=None) == fva.FVA_ERR_INVALID_ARG
+    assert Q(e=None) == fva.FVA_ERR_INVALID_ARG
+    assert Q(e=ctypes.c_void_p(0x7F0000001002)) == fva.FVA_ERR_INVALID_ARG  # v_exp not 4-byte aligned
+    assert Q(v8=ctypes.c_void_p(0x7F0000001008)) == fva.FVA_ERR_INVALID_ARG  # V8 not 16-byte aligned
+    assert Q(ws=None) == fva.FVA_ERR_WORKSPACE
+    assert Q(wsb=100) == fva.FVA_ERR_WORKSPACE
+    assert Q(dd=desc(N=10)) == fva.FVA_ERR_SHAPE
+    assert Q(dd=desc(D=64)) == fva.FVA_ERR_UNSUPPORTED
+    A = lambda v8=FAKE, e=FAKE, flags=0, wsb=1 << 40: L.fva_attn_fp8v(
+        FAKE, FAKE, v8, e, ctypes.byref(d), ctypes.byref(T720.c()), FAKE, None, None, ctypes.c_float(0.0), flags,
+        FAKE, FAKE, ctypes.c_size_t(wsb), None, None)
+    assert A(v8=None) == fva.FVA_ERR_INVALID_ARG
+    assert A(e=None) == fva.FVA_ERR_INVALID_ARG
+    assert A(flags=8) == fva.FVA_ERR_INVALID_ARG
+    assert A(wsb=10) == fva.FVA_ERR_WORKSPACE
+    assert L.fva_attn(FAKE, FAKE, None, ctypes.byref(d), ctypes.byref(T720.c()), FAKE, None, None,
+                      ctypes.c_float(0.0), 0, FAKE, FAKE, ctypes.c_size_t(1 << 40), None, None) == fva.FVA_ERR_INVALID_ARG
 
 
 def test_status_strings():
