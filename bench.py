@@ -163,23 +163,28 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 
 
 # HBM bytes per launch of attn_persistent_kernel on the 720p workload (3D
-# boxes, and Hilbert-curve blocks) from rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each scaled by the factor the same
+# boxes or Hilbert-curve blocks, bf16 or E4M3 V) from rocprofv3 FETCH_SIZE /
+# WRITE_SIZE passes, each scaled by the factor the same
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "2e8cc5e63181d037",
+    "source_digest": "24ec566bbaefdc1a",
     "bytes": {
-        "720p": (112363341 * 2 + 757141) * 1024,
-        "720p-hilbert": (89289480 * 2 + 757163) * 1024,
+        "720p": (117290198 * 2 + 757095) * 1024,
+        "720p-hilbert": (90766138 * 2 + 757275) * 1024,
+        "720p-fp8v": (71371828 * 2 + 758068) * 1024,
+        "720p-hilbert-fp8v": (68358685 * 2 + 758042) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "4a6577e51f087d77",
+    "source_digest": "efba76cc557ada31",
     "bytes": {
-        "720p": ((756175 + 29422 + 68204) * 2 + 53760 + 138978 + 49287) * 1024,
-        "720p-hilbert": ((756146 + 25769 + 55008) * 2 + 47360 + 112266 + 39990) * 1024,
+        "720p": ((756175 + 29387 + 68204) * 2 + 53760 + 138678 + 49287) * 1024,
+        "720p-hilbert": ((756147 + 25819 + 55008) * 2 + 47360 + 112511 + 39990) * 1024,
+        "720p-fp8v": ((756173 + 29402 + 68373) * 2 + 53760 + 138969 + 49300) * 1024,
+        "720p-hilbert-fp8v": ((756147 + 25744 + 55007) * 2 + 47360 + 112510 + 40000) * 1024,
     },
 }
 
