@@ -20,7 +20,9 @@ Balancing for Video Generation"):
 * block-sparse attention over the retained blocks only -- §2.1, §3.1;
 * the quantised-V variant (E4M3 codec, per-channel power-of-two scales,
   bound on the rounding of P) -- §3.4 (GPU-side V quantisation), in
-  fp8.py, imported on its own.
+  fp8.py, imported on its own;
+* slack-aware sparse augmentation (per-rank slack, trigger, budget, extra
+  blocks in the routing order) -- §3.3, in sasa.py, imported on its own.
 
 Parity status of each function is stated in its docstring. One part is
 "parity unpinned": whether these masks equal the masks of the paper's own
