@@ -252,6 +252,8 @@ def main():
     ap.add_argument("--sched", choices=["persistent", "naive"], default="persistent")
     ap.add_argument("--v", choices=["bf16", "fp8"], default="bf16", dest="vfmt",
                     help="attention on bf16 V, or on E4M3 V quantised inside the step")
+    ap.add_argument("--sasa", type=int, default=0, metavar="R",
+                    help="route with slack-aware augmentation over R ranks of contiguous heads (n1 0.8, n2 0.07)")
     ap.add_argument("--blocks", choices=["box", "hilbert"], default="box",
                     help="3D boxes, or runs of the Hilbert curve over curve-ordered tokens")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -316,6 +318,21 @@ def main():
         vexp = torch.empty((B, H, 128), dtype=torch.int32, device=dev)
         ws_q = torch.empty(fva.fva_quantize_v_workspace_size(desc, tiling), dtype=torch.uint8, device=dev)
 
+    if args.sasa:
+        R = args.sasa
+        if R < 1 or H % R:
+            raise SystemExit("--sasa R needs R to divide the number of heads")
+        rank_of = (torch.arange(B * H, device=dev, dtype=torch.int32) % H) // (H // R)
+        rank_extra = torch.empty(R, dtype=torch.int32, device=dev)
+        ws_r = torch.empty(fva.fva_route_sasa_workspace_size(desc, tiling), dtype=torch.uint8, device=dev)
+
+    def route(pp):
+        if args.sasa:
+            fva.fva_route_sasa(q, k, pp, cfg.k_min, tiling, rank_of, args.sasa, 0.8, 0.07, out=(mask, counts, kv),
+                               rank_extra=rank_extra, workspace=ws_r)
+        else:
+            fva.fva_route(q, k, pp, cfg.k_min, tiling, out=(mask, counts, kv), workspace=ws_r)
+
     def attend(fl, trace=None):
         if fp8:
             fva.fva_attn_fp8v(q, k, v8, vexp, tiling, mask, counts, kv, flags=fl, out=out, workspace=ws_a, trace=trace)
@@ -329,7 +346,7 @@ def main():
             fva.fva_quantize_v(v, tiling, out=(v8, vexp), workspace=ws_q)
         if ev:
             ev[3].record(stream)
-        fva.fva_route(q, k, pp, cfg.k_min, tiling, out=(mask, counts, kv), workspace=ws_r)
+        route(pp)
         if ev:
             ev[1].record(stream)
         attend(flags)
@@ -372,7 +389,8 @@ def main():
     shared = [os.path.join(csrc, f) for f in ("fva_common.h", "fva_geometry.h")]
     digest = source_digest(os.path.join(csrc, "attn_kernels.hip"), *shared)
     traffic = None
-    bench_workload = (cfg.name if curve is None else cfg.name + "-hilbert") + ("-fp8v" if fp8 else "")
+    bench_workload = ((cfg.name if curve is None else cfg.name + "-hilbert") + ("-fp8v" if fp8 else "")
+                      + (f"-sasa{args.sasa}" if args.sasa else ""))
     if ATTN_TRAFFIC["source_digest"] == digest and args.sched == "persistent":
         traffic = ATTN_TRAFFIC["bytes"].get(bench_workload)
     route_digest = source_digest(os.path.join(csrc, "route_kernels.hip"), *shared)
@@ -397,7 +415,8 @@ def main():
             "workload": f"{cfg.name}: {H} heads, d=128, latent grid {'x'.join(map(str, cfg.grid))} = {N} tokens, "
             + (f"tile {'x'.join(map(str, cfg.tile))}" if curve is None
                else f"Hilbert-curve blocks of {int(np.prod(cfg.tile))} tokens")
-            + f", nb={nb}, p={p}, k_min={cfg.k_min}" + (", E4M3 V (quantised each step)" if fp8 else ""),
+            + f", nb={nb}, p={p}, k_min={cfg.k_min}" + (", E4M3 V (quantised each step)" if fp8 else "")
+            + (f", slack-aware augmentation over {args.sasa} ranks of {H // args.sasa} heads" if args.sasa else ""),
             "blocks": args.blocks,
             "v": args.vfmt,
             "batch": B,
@@ -444,6 +463,29 @@ def main():
     }
     if curve is not None:
         res["curve_layout"] = curve
+    if args.sasa:
+        # loads before the augmentation, from a plain routing pass outside the timed region
+        c_aug = c_np.reshape(B * H, nb).astype(np.int64)
+        m0 = torch.empty_like(mask)
+        c0 = torch.empty_like(counts)
+        ws0 = torch.empty(fva.fva_route_workspace_size(desc, tiling), dtype=torch.uint8, device=dev)
+        fva.fva_route(q, k, p, cfg.k_min, tiling, out=(m0, c0, None), workspace=ws0)
+        torch.cuda.synchronize()
+        c_plain = c0.cpu().numpy().reshape(B * H, nb).astype(np.int64)
+        ro = rank_of.cpu().numpy()
+        S0 = np.bincount(ro, weights=c_plain.sum(axis=1), minlength=args.sasa) / nb
+        S1 = np.bincount(ro, weights=c_aug.sum(axis=1), minlength=args.sasa) / nb
+        res["sasa"] = {
+            "ranks": args.sasa, "n1": 0.8, "n2": 0.07,
+            "extra_blocks_per_row": rank_extra.cpu().numpy().tolist(),
+            "rank_load_rows_before": np.round(S0, 2).tolist(),
+            "rank_load_rows_after": np.round(S1, 2).tolist(),
+            "rho_before": round(float(S0.max() / S0.mean()), 4),
+            "rho_after": round(float(S1.max() / S1.mean()), 4),
+            "retained_before": round(float(c_plain.sum()) / (B * H * nb * nb), 4),
+            "retained_after": round(float(c_aug.sum()) / (B * H * nb * nb), 4),
+        }
+        log(f"[bench] sasa: {res['sasa']}")
     if not args.no_trace:
         tw = fva.fva_trace_words(desc, tiling)
         trace = torch.zeros(tw, dtype=torch.int64, device=dev)

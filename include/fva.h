@@ -121,6 +121,43 @@ fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, dou
                      void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Slack-aware sparse augmentation (§3.3), for the heads one GPU holds,
+ * grouped into ranks by rank_of.
+ *
+ * After routing as fva_route does, with S_h the sum of counts over head h's
+ * rows (nb * L_h of Eq. 1), S_r the sum of S_h over the heads of rank r and
+ * S_max = max_r S_r: a rank whose slack D_r = S_max - S_r passes the trigger
+ * D_r > n2 * S_max (the paper's threshold n2 on the slack) gets the budget
+ * n1 * D_r / nb rows of work (the budget B_r = n1 * slack), spent evenly:
+ * every row of its H_r heads keeps
+ *   e_r = floor((n1 * D_r) / (nb * H_r))
+ * more key blocks, the next ones in the routing order (score descending,
+ * ties to the lower id); a row never keeps more than nb. The trigger and
+ * e_r are evaluated in fp64 exactly as written, from exact integer sums, so
+ * the result is deterministic; the rank loads S_r + H_r * nb * e_r never
+ * exceed S_max (no new straggler, n1 <= 1).
+ */
+/* Workspace of fva_route_sasa: that of fva_route plus batch*heads int32,
+ * 256-byte aligned. Host only. */
+fva_status fva_route_sasa_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes);
+
+/*
+ * fva_route_sasa -- fva_route followed by the augmentation above.
+ * rank_of: device int32 [batch * heads], the rank of head (b, h) at index
+ *          b * heads + h; heads with an id outside [0, n_ranks) take no
+ *          part (no load, no extra blocks).
+ * n_ranks in [1, 1024]; n1, n2 in [0, 1] (the paper uses 0.8 and 0.07).
+ * Outputs as for fva_route (after augmentation); rank_extra: device int32
+ *          [n_ranks] = e_r, or NULL.
+ * Errors as for fva_route; FVA_ERR_INVALID_ARG for a NULL or misaligned
+ * rank_of, n_ranks or n1 / n2 out of range.
+ */
+fva_status fva_route_sasa(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
+                          const fva_tiling* tiling, const int32_t* rank_of, int32_t n_ranks, double n1, double n2,
+                          uint8_t* block_mask, int32_t* counts, int32_t* kv_idx, int32_t* rank_extra, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/*
  * Workspace bytes needed by fva_attn for this shape and flags: the work
  * list and queue counters, room for counts and kv_idx (batch*heads*nb and
  * batch*heads*nb*nb int32) used when the caller passes them as NULL, one

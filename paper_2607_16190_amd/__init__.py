@@ -50,6 +50,8 @@ EXPORTED = (
     "fva_num_blocks",
     "fva_route_workspace_size",
     "fva_route",
+    "fva_route_sasa_workspace_size",
+    "fva_route_sasa",
     "fva_attn_workspace_size",
     "fva_trace_words",
     "fva_attn",
@@ -132,6 +134,12 @@ def _load():
         "fva_route": (
             ctypes.c_int,
             [P, P, D, ctypes.c_double, ctypes.c_int32, T, P, P, P, P, ctypes.c_size_t, P],
+        ),
+        "fva_route_sasa_workspace_size": (ctypes.c_int, [D, T, sz]),
+        "fva_route_sasa": (
+            ctypes.c_int,
+            [P, P, D, ctypes.c_double, ctypes.c_int32, T, P, ctypes.c_int32, ctypes.c_double, ctypes.c_double, P, P,
+             P, P, P, ctypes.c_size_t, P],
         ),
         "fva_attn_workspace_size": (ctypes.c_int, [D, T, ctypes.c_uint32, sz]),
         "fva_trace_words": (ctypes.c_int64, [D, T]),
@@ -244,6 +252,49 @@ def fva_route(q, k, p: float, k_min: int, tiling: Tiling, *, kv_idx: bool = True
     )
     _check(st, "fva_route")
     return mask, counts, kv
+
+
+def fva_route_sasa_workspace_size(desc: _Desc, tiling: Tiling) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.fva_route_sasa_workspace_size(ctypes.byref(desc), ctypes.byref(tiling.c()), ctypes.byref(n)),
+           "fva_route_sasa_workspace_size")
+    return n.value
+
+
+def fva_route_sasa(q, k, p: float, k_min: int, tiling: Tiling, rank_of, n_ranks: int, n1: float = 0.8,
+                   n2: float = 0.07, *, kv_idx: bool = True, out=None, rank_extra=None, workspace=None, stream=None):
+    """Routing plus slack-aware augmentation over the ranks of rank_of (see include/fva.h).
+
+    rank_of: int32 device tensor [batch * heads]. Returns (mask, counts, kv_idx or None, rank_extra).
+    """
+    import torch
+
+    if q.dtype != torch.bfloat16 or k.dtype != torch.bfloat16 or not q.is_cuda or not k.is_cuda:
+        raise ValueError("q and k must be bf16 device tensors")
+    if q.shape != k.shape or q.stride() != k.stride():
+        raise ValueError("q and k must share shape and strides")
+    if (rank_of.dtype != torch.int32 or not rank_of.is_cuda or not rank_of.is_contiguous()
+            or rank_of.numel() != q.shape[0] * q.shape[1]):
+        raise ValueError("rank_of must be a contiguous int32 device tensor with one entry per (batch, head)")
+    desc = _desc_of(q)
+    nb = fva_num_blocks(tiling)
+    B, H = q.shape[0], q.shape[1]
+    if out is None:
+        mask = torch.empty((B, H, max(nb, 0), max(nb, 0)), dtype=torch.uint8, device=q.device)
+        counts = torch.empty((B, H, max(nb, 0)), dtype=torch.int32, device=q.device)
+        kv = torch.empty((B, H, max(nb, 0), max(nb, 0)), dtype=torch.int32, device=q.device) if kv_idx else None
+    else:
+        mask, counts, kv = out
+    if rank_extra is None:
+        rank_extra = torch.empty(max(int(n_ranks), 1), dtype=torch.int32, device=q.device)
+    ws = _workspace(torch, fva_route_sasa_workspace_size(desc, tiling), q.device, workspace)
+    st = lib.fva_route_sasa(
+        _ptr(q), _ptr(k), ctypes.byref(desc), float(p), int(k_min), ctypes.byref(tiling.c()), _ptr(rank_of),
+        int(n_ranks), float(n1), float(n2), _ptr(mask), _ptr(counts), _ptr(kv), _ptr(rank_extra), _ptr(ws),
+        ctypes.c_size_t(ws.numel() * ws.element_size()), _stream_ptr(torch, stream),
+    )
+    _check(st, "fva_route_sasa")
+    return mask, counts, kv, rank_extra
 
 
 def fva_attn(q, k, v, tiling: Tiling, mask, counts=None, kv_idx=None, *, scale: float = 0.0, flags: int = 0,

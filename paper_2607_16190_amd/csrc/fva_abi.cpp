@@ -86,16 +86,22 @@ int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling) {
   return fva::attn_trace_words(desc->batch, desc->heads, nb);
 }
 
-fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
-                     const fva_tiling* tiling, uint8_t* block_mask, int32_t* counts, int32_t* kv_idx, void* workspace,
-                     size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+fva_status route_common(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
+                        const fva_tiling* tiling, uint8_t* block_mask, int32_t* counts, int32_t* kv_idx,
+                        const int32_t* rank_of, int32_t n_ranks, double n1, double n2, int32_t* rank_extra,
+                        void* workspace, size_t workspace_bytes, void* stream) {
   if (!Q || !K || !block_mask || !counts) return FVA_ERR_INVALID_ARG;
   if (std::isnan(p) || p < 0.0 || p > 1.0 || k_min < 0) return FVA_ERR_INVALID_ARG;
   int nb = 0;
   const fva_status s = check_shape(desc, tiling, &nb);
   if (s != FVA_OK) return s;
   if (!aligned16(Q) || !aligned16(K)) return FVA_ERR_INVALID_ARG;
-  const size_t need = fva::route_workspace_bytes(desc->batch, desc->heads, nb);
+  const size_t need = rank_of ? fva::route_sasa_workspace_bytes(desc->batch, desc->heads, nb)
+                              : fva::route_workspace_bytes(desc->batch, desc->heads, nb);
   if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;
   fva::RouteArgs a;
   a.Q = Q;
@@ -117,9 +123,46 @@ fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, dou
   a.mask = block_mask;
   a.counts = counts;
   a.kv_idx = kv_idx;
+  a.rank_of = rank_of;
+  a.n_ranks = n_ranks;
+  a.n1 = n1;
+  a.n2 = n2;
+  a.rank_extra = rank_extra;
   a.workspace = workspace;
   a.stream = reinterpret_cast<hipStream_t>(stream);
   return fva::launch_route(a) == hipSuccess ? FVA_OK : FVA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
+                     const fva_tiling* tiling, uint8_t* block_mask, int32_t* counts, int32_t* kv_idx, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  return route_common(Q, K, desc, p, k_min, tiling, block_mask, counts, kv_idx, nullptr, 0, 0.0, 0.0, nullptr,
+                      workspace, workspace_bytes, stream);
+}
+
+fva_status fva_route_sasa_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes) {
+  if (!bytes) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  *bytes = fva::route_sasa_workspace_bytes(desc->batch, desc->heads, nb);
+  return FVA_OK;
+}
+
+fva_status fva_route_sasa(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
+                          const fva_tiling* tiling, const int32_t* rank_of, int32_t n_ranks, double n1, double n2,
+                          uint8_t* block_mask, int32_t* counts, int32_t* kv_idx, int32_t* rank_extra, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  if (!rank_of || (reinterpret_cast<uintptr_t>(rank_of) & 3u)) return FVA_ERR_INVALID_ARG;
+  if (rank_extra && (reinterpret_cast<uintptr_t>(rank_extra) & 3u)) return FVA_ERR_INVALID_ARG;
+  if (n_ranks < 1 || n_ranks > 1024) return FVA_ERR_INVALID_ARG;
+  if (!(n1 >= 0.0 && n1 <= 1.0) || !(n2 >= 0.0 && n2 <= 1.0)) return FVA_ERR_INVALID_ARG;
+  return route_common(Q, K, desc, p, k_min, tiling, block_mask, counts, kv_idx, rank_of, n_ranks, n1, n2, rank_extra,
+                      workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -18,6 +18,12 @@ struct RouteArgs {
   uint8_t* mask;
   int32_t* counts;
   int32_t* kv_idx;  // may be null
+  // slack-aware augmentation (null rank_of: plain routing)
+  const int32_t* rank_of = nullptr;  // [batch * heads] rank of every head (device)
+  int n_ranks = 0;
+  double n1 = 0.0, n2 = 0.0;
+  int32_t* rank_extra = nullptr;  // [n_ranks] extra blocks per row of each rank (device) or null
+  int32_t* extra_head = nullptr;  // [batch * heads] workspace tail
   void* workspace;
   hipStream_t stream;
 };
@@ -54,6 +60,7 @@ struct QuantizeArgs {
 };
 
 size_t route_workspace_bytes(int batch, int heads, int nb);
+size_t route_sasa_workspace_bytes(int batch, int heads, int nb);
 size_t attn_workspace_bytes(int batch, int heads, int nb, uint32_t flags);
 int64_t attn_trace_words(int batch, int heads, int nb);
 

@@ -353,9 +353,10 @@ __device__ Cut select_cut(const double (&s)[KPL], const uint64_t (&F)[KPL], uint
 }
 
 template <int KPL>
-__device__ void select_row(const double* __restrict__ srow, int nb, double p, int k_min, uint8_t* __restrict__ mrow,
-                           int32_t* __restrict__ count_out, int32_t* __restrict__ kvrow, WaveScratch& ws,
-                           int lane) {
+__device__ __forceinline__ void select_row(const double* __restrict__ srow, int nb, double p, int k_min,
+                                           uint8_t* __restrict__ mrow, int32_t* __restrict__ count_out,
+                                           int32_t* __restrict__ kvrow, WaveScratch& ws, int lane,
+                                           int m_force = -1) {
   double s[KPL];
   uint64_t F[KPL];
   uint32_t valid = 0;
@@ -399,7 +400,10 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
   cut.j = -1;
   cut.s = 0.0;
   cut.rank = 0;
-  if (p >= 1.0) {
+  if (m_force >= 0) {
+    // a given count: the first m_force blocks of the same order
+    m_p = m_force < nb ? m_force : nb;
+  } else if (p >= 1.0) {
     m_p = nb;
   } else {
     const uint64_t T = (uint64_t)ceil(p * kMassScale);
@@ -412,8 +416,9 @@ __device__ void select_row(const double* __restrict__ srow, int nb, double p, in
       m_p = cut.rank;
     }
   }
-  const int m = m_p > kf ? m_p : kf;
-  if (m > 0 && m < nb && m != m_p) cut = select_cut<KPL>(s, F, valid, nb, smin, smax, zs, false, (uint64_t)m, ws, lane);
+  const int m = m_force >= 0 ? m_p : (m_p > kf ? m_p : kf);
+  if (m > 0 && m < nb && (m != m_p || m_force >= 0))
+    cut = select_cut<KPL>(s, F, valid, nb, smin, smax, zs, false, (uint64_t)m, ws, lane);
 
   // Kept blocks: the first m of (score desc, id asc), i.e. those ahead of or
   // equal to the cut block.
@@ -561,11 +566,97 @@ __global__ __launch_bounds__(64 * kRowWaves, KPL > 12 ? 3 : 4) void select_kerne
                   wsa[wave], lane);
 }
 
+// Slack-aware augmentation, second pass: a row of a head with extra[h] > 0
+// blocks keeps the first min(nb, counts + extra) blocks of the same order
+// (the scores are those of the first pass); other rows are left as they are.
+template <int KPL>
+__global__ __launch_bounds__(64 * kRowWaves, KPL > 12 ? 3 : 4) void augment_kernel(
+    const double* __restrict__ scores, int nb, int64_t nrows, const int32_t* __restrict__ extra,
+    uint8_t* __restrict__ mask, int32_t* __restrict__ counts, int32_t* __restrict__ kv_idx) {
+  __shared__ WaveScratch wsa[kRowWaves];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t row = (int64_t)blockIdx.x * kRowWaves + wave;
+  if (row >= nrows) return;
+  const int e = __builtin_amdgcn_readfirstlane(extra[row / nb]);
+  if (e <= 0) return;
+  const int m0 = __builtin_amdgcn_readfirstlane(counts[row]);
+  const int m = (int)min((int64_t)nb, (int64_t)max(m0, 0) + e);
+  select_row<KPL>(scores + row * nb, nb, 0.0, 0, mask + row * nb, counts + row, kv_idx ? kv_idx + row * nb : nullptr,
+                  wsa[wave], lane, m);
+}
+
+// Slack-aware augmentation, budget (one workgroup): S_h = kept blocks of head
+// h over its rows, S_r = sum over the heads of rank r (exact integers),
+// S_max = max_r S_r; a rank whose slack D = S_max - S_r passes the trigger
+// D > n2 * S_max gets floor(n1 * D / (nb * H_r)) extra blocks per row (H_r
+// heads). Heads with a rank id outside [0, n_ranks) take no part.
+constexpr int kMaxRanks = 1024;
+
+__global__ __launch_bounds__(1024) void sasa_budget_kernel(const int32_t* __restrict__ counts, int n_heads, int nb,
+                                                           const int32_t* __restrict__ rank_of, int n_ranks,
+                                                           double n1, double n2, int32_t* __restrict__ extra_head,
+                                                           int32_t* __restrict__ rank_extra) {
+  __shared__ unsigned long long S_r[kMaxRanks];
+  __shared__ int H_r[kMaxRanks];
+  __shared__ int ex_r[kMaxRanks];
+  __shared__ unsigned long long S_max;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  for (int r = threadIdx.x; r < n_ranks; r += blockDim.x) {
+    S_r[r] = 0ull;
+    H_r[r] = 0;
+  }
+  __syncthreads();
+  for (int h = wave; h < n_heads; h += nwaves) {
+    unsigned long long sum = 0ull;
+    for (int i = lane; i < nb; i += 64) {
+      const int c = counts[(int64_t)h * nb + i];
+      sum += (unsigned long long)(c < 0 ? 0 : (c > nb ? nb : c));
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+    const int r = rank_of[h];
+    if (lane == 0 && r >= 0 && r < n_ranks) {
+      atomicAdd(&S_r[r], sum);
+      atomicAdd(&H_r[r], 1);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long mx = 0ull;
+    for (int r = 0; r < n_ranks; ++r) mx = S_r[r] > mx ? S_r[r] : mx;
+    S_max = mx;
+  }
+  __syncthreads();
+  for (int r = threadIdx.x; r < n_ranks; r += blockDim.x) {
+    const unsigned long long D = S_max - S_r[r];
+    int e = 0;
+    if (H_r[r] > 0 && (double)D > n2 * (double)S_max) e = (int)floor((n1 * (double)D) / (double)(nb * H_r[r]));
+    ex_r[r] = e;
+    if (rank_extra) rank_extra[r] = e;
+  }
+  __syncthreads();
+  for (int h = threadIdx.x; h < n_heads; h += blockDim.x) {
+    const int r = rank_of[h];
+    extra_head[h] = (r >= 0 && r < n_ranks) ? ex_r[r] : 0;
+  }
+}
+
 template <int KPL>
 hipError_t launch_select(const RouteArgs& a, int nb, const double* scores) {
   const int64_t nrows = (int64_t)a.batch * a.heads * nb;
   const dim3 grid((unsigned)((nrows + kRowWaves - 1) / kRowWaves));
   hipLaunchKernelGGL(select_kernel<KPL>, grid, dim3(64 * kRowWaves), 0, a.stream, scores, nb, nrows, a.p, a.k_min,
+                     a.mask, a.counts, a.kv_idx);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !a.rank_of) return e;
+  hipLaunchKernelGGL(sasa_budget_kernel, dim3(1), dim3(1024), 0, a.stream, a.counts, a.batch * a.heads, nb, a.rank_of,
+                     a.n_ranks, a.n1, a.n2, a.extra_head, a.rank_extra);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(augment_kernel<KPL>, grid, dim3(64 * kRowWaves), 0, a.stream, scores, nb, nrows, a.extra_head,
                      a.mask, a.counts, a.kv_idx);
   return hipGetLastError();
 }
@@ -590,6 +681,10 @@ size_t route_workspace_bytes(int batch, int heads, int nb) {
   return 2 * w.means + w.scores;
 }
 
+size_t route_sasa_workspace_bytes(int batch, int heads, int nb) {
+  return route_workspace_bytes(batch, heads, nb) + (((size_t)batch * heads * 4 + 255) & ~(size_t)255);
+}
+
 hipError_t launch_route(const RouteArgs& a) {
   (void)hipGetLastError();  // drop an error left by an unrelated earlier HIP call
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
@@ -600,6 +695,8 @@ hipError_t launch_route(const RouteArgs& a) {
   double* qbar = reinterpret_cast<double*>(base);
   double* kbar = reinterpret_cast<double*>(base + w.means);
   double* scores = reinterpret_cast<double*>(base + 2 * w.means);
+  RouteArgs args = a;
+  if (a.rank_of) args.extra_head = reinterpret_cast<int32_t*>(base + 2 * w.means + w.scores);
   hipLaunchKernelGGL(pool_kernel, dim3(padded_blocks(g.nb) / kPoolBlocks, bhs), dim3(kPoolThreads), 0, a.stream,
                      reinterpret_cast<const uint16_t*>(a.Q), reinterpret_cast<const uint16_t*>(a.K), a.heads,
                      a.stride_b, a.stride_h, a.stride_n, g, qbar, kbar);
@@ -610,11 +707,11 @@ hipError_t launch_route(const RouteArgs& a) {
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int kpl = (g.nb + 63) / 64;
-  if (kpl <= 2) return launch_select<2>(a, g.nb, scores);
-  if (kpl <= 4) return launch_select<4>(a, g.nb, scores);
-  if (kpl <= 8) return launch_select<8>(a, g.nb, scores);
-  if (kpl <= 12) return launch_select<12>(a, g.nb, scores);
-  return launch_select<16>(a, g.nb, scores);
+  if (kpl <= 2) return launch_select<2>(args, g.nb, scores);
+  if (kpl <= 4) return launch_select<4>(args, g.nb, scores);
+  if (kpl <= 8) return launch_select<8>(args, g.nb, scores);
+  if (kpl <= 12) return launch_select<12>(args, g.nb, scores);
+  return launch_select<16>(args, g.nb, scores);
 }
 
 }  // namespace fva

@@ -205,6 +205,26 @@ def test_fp8_sizes_and_argument_errors():
                       ctypes.c_float(0.0), 0, FAKE, FAKE, ctypes.c_size_t(1 << 40), None, None) == fva.FVA_ERR_INVALID_ARG
 
 
+def test_route_sasa_sizes_and_argument_errors():
+    d = desc()
+    assert fva.fva_route_sasa_workspace_size(d, T720) == fva.fva_route_workspace_size(d, T720) + 256  # 40 int32
+    L = fva.lib
+    R = lambda rank_of=FAKE, n=8, n1=0.8, n2=0.07, ws=FAKE, wsb=1 << 40, extra=None: L.fva_route_sasa(
+        FAKE, FAKE, ctypes.byref(d), 0.9, 4, ctypes.byref(T720.c()), rank_of, n, n1, n2, FAKE, FAKE, None, extra,
+        ws, ctypes.c_size_t(wsb), None)
+    assert R(rank_of=None) == fva.FVA_ERR_INVALID_ARG
+    assert R(rank_of=ctypes.c_void_p(0x7F0000001002)) == fva.FVA_ERR_INVALID_ARG
+    assert R(extra=ctypes.c_void_p(0x7F0000001001)) == fva.FVA_ERR_INVALID_ARG
+    assert R(n=0) == fva.FVA_ERR_INVALID_ARG
+    assert R(n=1025) == fva.FVA_ERR_INVALID_ARG
+    assert R(n1=-0.1) == fva.FVA_ERR_INVALID_ARG
+    assert R(n1=1.5) == fva.FVA_ERR_INVALID_ARG
+    assert R(n1=float("nan")) == fva.FVA_ERR_INVALID_ARG
+    assert R(n2=2.0) == fva.FVA_ERR_INVALID_ARG
+    plain = fva.fva_route_workspace_size(d, T720)
+    assert R(wsb=plain) == fva.FVA_ERR_WORKSPACE  # the augmentation needs the tail
+
+
 def test_status_strings():
     assert fva.fva_status_string(0) == "ok"
     for s in (-1, -2, -3, -4, -5):
