@@ -469,8 +469,35 @@ def main():
         m0 = torch.empty_like(mask)
         c0 = torch.empty_like(counts)
         ws0 = torch.empty(fva.fva_route_workspace_size(desc, tiling), dtype=torch.uint8, device=dev)
-        fva.fva_route(q, k, p, cfg.k_min, tiling, out=(m0, c0, None), workspace=ws0)
+        kv0 = torch.empty_like(kv)
+        fva.fva_route(q, k, p, cfg.k_min, tiling, out=(m0, c0, kv0), workspace=ws0)
         torch.cuda.synchronize()
+
+        def rank_times(mm, cc, kk, reps=3):
+            """Attention time of each rank's heads alone (what that rank's GPU would run)."""
+            hp = H // args.sasa
+            out_t = []
+            for r in range(args.sasa):
+                sl = slice(r * hp, (r + 1) * hp)
+                qs, ks_, vs = q[:, sl], k[:, sl], v[:, sl]
+                ms, cs, kvs = mm[:, sl], cc[:, sl], kk[:, sl]
+                o_s = torch.empty_strided(qs.shape, qs.stride(), dtype=torch.bfloat16, device=dev)
+                if fp8:
+                    v8s, vexps = v8[:, sl], vexp[:, sl]
+                    fn = lambda: fva.fva_attn_fp8v(qs, ks_, v8s.contiguous(), vexps.contiguous(), tiling, ms, cs, kvs,
+                                                   out=o_s, workspace=ws_a)
+                else:
+                    fn = lambda: fva.fva_attn(qs, ks_, vs, tiling, ms, cs, kvs, out=o_s, workspace=ws_a)
+                fn()
+                torch.cuda.synchronize()
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                ev[0].record(stream)
+                for _ in range(reps):
+                    fn()
+                ev[1].record(stream)
+                torch.cuda.synchronize()
+                out_t.append(ev[0].elapsed_time(ev[1]) / reps)
+            return out_t
         c_plain = c0.cpu().numpy().reshape(B * H, nb).astype(np.int64)
         ro = rank_of.cpu().numpy()
         S0 = np.bincount(ro, weights=c_plain.sum(axis=1), minlength=args.sasa) / nb
@@ -485,6 +512,12 @@ def main():
             "retained_before": round(float(c_plain.sum()) / (B * H * nb * nb), 4),
             "retained_after": round(float(c_aug.sum()) / (B * H * nb * nb), 4),
         }
+        if B == 1:
+            t0 = rank_times(m0, c0, kv0)
+            t1 = rank_times(mask, counts, kv)
+            res["sasa"]["rank_attn_ms_before"] = [round(x, 3) for x in t0]
+            res["sasa"]["rank_attn_ms_after"] = [round(x, 3) for x in t1]
+            res["sasa"]["critical_attn_ms_before_after"] = [round(max(t0), 3), round(max(t1), 3)]
         log(f"[bench] sasa: {res['sasa']}")
     if not args.no_trace:
         tw = fva.fva_trace_words(desc, tiling)
