@@ -179,12 +179,12 @@ ATTN_TRAFFIC = {
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "efba76cc557ada31",
+    "source_digest": "bcd080cb3a00db2b",
     "bytes": {
-        "720p": ((756175 + 29387 + 68204) * 2 + 53760 + 138678 + 49287) * 1024,
-        "720p-hilbert": ((756147 + 25819 + 55008) * 2 + 47360 + 112511 + 39990) * 1024,
-        "720p-fp8v": ((756173 + 29402 + 68373) * 2 + 53760 + 138969 + 49300) * 1024,
-        "720p-hilbert-fp8v": ((756147 + 25744 + 55007) * 2 + 47360 + 112510 + 40000) * 1024,
+        "720p": ((756149 + 29557 + 68204) * 2 + 53760 + 138818 + 49287) * 1024,
+        "720p-hilbert": ((756148 + 25799 + 55008) * 2 + 47360 + 112437 + 39990) * 1024,
+        "720p-fp8v": ((756172 + 29276 + 68204) * 2 + 53760 + 139059 + 49286) * 1024,
+        "720p-hilbert-fp8v": ((756147 + 25694 + 55009) * 2 + 47360 + 112567 + 39990) * 1024,
     },
 }
 
