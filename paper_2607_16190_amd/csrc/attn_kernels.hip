@@ -441,7 +441,8 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   // Online softmax over the half. Accumulator (t, r) of lane group g4 holds
   // key 64hb + 32*(t/2) + 8*g4 + 4*(t%2) + r; keys past nj are masked (in a
   // short half that covers every key of tiles 2 and 3).
-  auto softmax_phase = [&](int hb, bool short_half, int nj, f32x4 (&s)[4][2], bf16x8 (&pb)[2][2]) {
+  auto softmax_phase = [&](int hb, bool short_half, int nj, f32x4 (&s)[4][2], bf16x8 (&pb)[2][2],
+                           float (&negm)[2]) {
     if (nj < 64 * hb + 64) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
@@ -487,30 +488,28 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
         }
       }
     }
-    const float negm[2] = {-mrow[0] * P.c2, -mrow[1] * P.c2};
-    auto group = [&](auto kk_c) {
-      constexpr int kk = decltype(kk_c)::value;
+    negm[0] = -mrow[0] * P.c2;
+    negm[1] = -mrow[1] * P.c2;
+    // The first 32 keys only: the exponentials of the second 32 are taken
+    // inside the PV phase, under the products of the first.
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int t = 2 * kk + hh;
+    for (int t = 0; t < 2; ++t) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
+      for (int r = 0; r < 4; ++r) {
 #pragma unroll
-          for (int nt = 0; nt < 2; ++nt) {
-            s[t][nt][r] = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
-          }
-        }
+        for (int nt = 0; nt < 2; ++nt) s[t][nt][r] = __builtin_amdgcn_exp2f(fmaf(s[t][nt][r], P.c2, negm[nt]));
       }
-      pb[kk][0] = to_bf16x8(s[2 * kk][0], s[2 * kk + 1][0]);
-      pb[kk][1] = to_bf16x8(s[2 * kk][1], s[2 * kk + 1][1]);
-    };
-    group(std::integral_constant<int, 0>{});
-    if (!short_half) group(std::integral_constant<int, 1>{});
+    }
+    pb[0][0] = to_bf16x8(s[0][0], s[1][0]);
+    pb[0][1] = to_bf16x8(s[0][1], s[1][1]);
+    (void)short_half;
   };
 
   // O^T += V^T P^T, 32 keys per MFMA; V^T comes from row-major V through
-  // transposing LDS reads. Step u = 8kk + mt.
-  auto pv_phase = [&](int hb, bool short_half, const bf16x8 (&pb)[2][2]) {
+  // transposing LDS reads. Step u = 8kk + mt. Steps 0..7 (the first 32 keys)
+  // also take the exponentials of the second 32 keys, two values a step, so
+  // that VALU work runs while the matrix unit multiplies.
+  auto pv_phase = [&](int hb, bool short_half, bf16x8 (&pb)[2][2], f32x4 (&s)[4][2], const float (&negm)[2]) {
     constexpr int kVPre = 3;
     bf16x8 vq[kVPre + 1];
 #pragma unroll
@@ -526,6 +525,20 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
       if (mt == 7) {
         lsum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][0], lsum[0], 0, 0, 0);
         lsum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kk][1], lsum[1], 0, 0, 0);
+      }
+      if constexpr (u < 8) {
+        // values 2u, 2u + 1 of the second group: tile 2 + u / 4, row u % 4, both query tiles
+        if (!short_half) {
+          constexpr int t = 2 + (u >> 2), r = u & 3;
+          s[t][0][r] = __builtin_amdgcn_exp2f(fmaf(s[t][0][r], P.c2, negm[0]));
+          s[t][1][r] = __builtin_amdgcn_exp2f(fmaf(s[t][1][r], P.c2, negm[1]));
+        }
+        if constexpr (u == 7) {
+          if (!short_half) {
+            pb[1][0] = to_bf16x8(s[2][0], s[3][0]);
+            pb[1][1] = to_bf16x8(s[2][1], s[3][1]);
+          }
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     };
@@ -719,6 +732,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
       const bool short_half = hb == 1 && ng == 3;
       f32x4 s[4][2];
       bf16x8 pb[2][2];
+      float negm[2];
       if (active && run) s_phase(hb, short_half, s);
       if (hb == 0) {
         // record of block c + 1 and the id of block c + 2 (clamped to the list)
@@ -737,7 +751,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
           }
         }
       }
-      if (active && run) softmax_phase(hb, short_half, nj, s, pb);
+      if (active && run) softmax_phase(hb, short_half, nj, s, pb, negm);
       if (hb == 0) {
         // The prefetched scalars have landed long ago; waiting for them here,
         // where no LDS read is in flight, keeps the PV fragment waits exact.
@@ -746,7 +760,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
         wait_vmem<0>();
         tile_barrier();
       }
-      if (active && run) pv_phase(hb, short_half, pb);
+      if (active && run) pv_phase(hb, short_half, pb, s, negm);
     }
     tile_barrier();  // every wave is done with V_c
     if (c + 1 < cnt && wave < ng_next) issue_tile<true>(Vh, roff, Vs);
