@@ -168,12 +168,12 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "24ec566bbaefdc1a",
+    "source_digest": "bea204804a891f72",
     "bytes": {
-        "720p": (117290198 * 2 + 757095) * 1024,
-        "720p-hilbert": (90766138 * 2 + 757275) * 1024,
-        "720p-fp8v": (71371828 * 2 + 758068) * 1024,
-        "720p-hilbert-fp8v": (68358685 * 2 + 758042) * 1024,
+        "720p": (116721688 * 2 + 757109) * 1024,
+        "720p-hilbert": (79169325 * 2 + 757235) * 1024,
+        "720p-fp8v": (71441940 * 2 + 758050) * 1024,
+        "720p-hilbert-fp8v": (68150692 * 2 + 758019) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
