@@ -155,3 +155,18 @@ def test_curve_route_attn_full_workloads(name):
     e = np.concatenate(errs)
     log(f"[curve] {name} attn: heads {heads}, max abs {e.max():.3e} mean abs {e.mean():.3e}")
     assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
+
+
+def test_permute_rows_batch_two_bhnd_layout():
+    # [batch, tokens, heads, 128] storage viewed as [batch, heads, tokens, 128]
+    fva, torch = lib(), torch_mod()
+    N, H = 500, 3
+    g = torch.Generator().manual_seed(6)
+    store = torch.randn(2, N, H, 128, generator=g).to(torch.bfloat16).to("cuda:0")
+    x = store.permute(0, 2, 1, 3)
+    perm = torch.randperm(N, generator=g).to(torch.int32)
+    y = fva.fva_permute_tokens(x, perm.to("cuda:0"), fva.FVA_TO_CURVE)
+    torch.cuda.synchronize()
+    xb = bits16(x)
+    assert y.stride() == x.stride()
+    assert np.array_equal(bits16(y), xb[:, :, perm.numpy().astype(np.int64)])

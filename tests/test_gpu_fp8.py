@@ -184,3 +184,47 @@ def test_fp8_attn_deterministic():
     O1 = fp8_attn(Qb, Kb, Vb, tiling, mask, counts, kv)
     O2 = fp8_attn(Qb, Kb, Vb, tiling, mask, counts, kv)
     assert np.array_equal(O1, O2)
+
+
+@pytest.mark.parametrize("name,B", [("tiny", 64), ("480p", 128)])
+def test_fp8_attn_hilbert_blocks(name, B):
+    # curve order + E4M3 V: the whole variant stack, against the oracle on
+    # curve blocks and dequantised V (raster order), under the same bar
+    fva, torch = lib(), torch_mod()
+    cfg = synth.get_config(name)
+    Qb, Kb, Vb = workload(name)
+    geo = curve_geometry(*cfg.grid, B)
+    q, k, v = to_dev(Qb), to_dev(Kb), to_dev(Vb)
+    perm = fva.fva_curve_order(*cfg.grid, device="cuda:0")
+    qc, kc, vc = (fva.fva_permute_tokens(t, perm, fva.FVA_TO_CURVE) for t in (q, k, v))
+    tc = fva.Tiling.curve(cfg.N, B)
+    mask, counts, kv = fva.fva_route(qc, kc, cfg.p, cfg.k_min, tc)
+    v8, vexp = fva.fva_quantize_v(vc, tc)
+    oc = fva.fva_attn_fp8v(qc, kc, v8, vexp, tc, mask, counts, kv)
+    O = fva.fva_permute_tokens(oc, perm, fva.FVA_FROM_CURVE).float().cpu().numpy().astype(np.float64)
+    torch.cuda.synchronize()
+    m = mask.cpu().numpy()[0]
+    # the quantiser saw the permuted rows, whose channel maxima are the same
+    assert np.array_equal(vexp.cpu().numpy()[0], np.stack([quantize_v(f64(Vb[0, h]))[1] for h in range(cfg.heads)]))
+    rng = np.random.default_rng(37)
+    heads = range(cfg.heads) if cfg.heads <= 2 else [0, int(rng.integers(cfg.heads))]
+    rows = {h: (list(range(geo.nb)) if geo.nb <= 16 else
+                sorted({int(i) for i in rng.choice(geo.nb, 3, replace=False)} | {geo.nb - 1})) for h in heads}
+    compare_rows(f"{name} hilbert", Qb, Kb, Vb, m, O[0], geo, rows)
+
+
+def test_fp8_attn_batch_two_odd_heads():
+    fva, torch = lib(), torch_mod()
+    cfg = synth.WorkloadConfig("fp8b2", 3, (5, 13, 21), (2, 8, 8), 0.9, 3, 19, "fixed", (0.7, 2.5, 4.0), batch=2)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    geo = geometry_of(cfg)
+    t = tiling_of(cfg)
+    q, k, v = to_dev(Qb), to_dev(Kb), to_dev(Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, t)
+    v8, vexp = fva.fva_quantize_v(v, t)
+    O = fva.fva_attn_fp8v(q, k, v8, vexp, t, mask, counts, kv).float().cpu().numpy().astype(np.float64)
+    torch.cuda.synchronize()
+    for b in range(2):
+        sel = lambda X: X[b:b + 1]
+        compare_rows(f"batch {b}", sel(Qb), sel(Kb), sel(Vb), mask.cpu().numpy()[b], O[b], geo,
+                     {h: list(range(geo.nb)) for h in range(3)})

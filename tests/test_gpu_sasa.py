@@ -90,3 +90,22 @@ def test_sasa_heads_without_rank_and_empty_rank():
     Qb, Kb, _ = synth.gen_qkv(cfg)
     # head 1 has no rank (-1), head 3 an id past n_ranks; rank 2 holds no head
     check("no-rank", Qb, Kb, cfg, [0, -1, 1, 7], 3, n1=0.9, n2=0.0)
+
+
+def test_sasa_batch_two():
+    # ranks over batch * heads: rank_of[b * heads + h]
+    fva, torch = lib(), torch_mod()
+    cfg = synth.WorkloadConfig("sasab2", 3, (3, 16, 16), (1, 8, 8), 0.9, 2, 47, "fixed", (0.3, 5.0, 2.0), batch=2)
+    Qb, Kb, _ = synth.gen_qkv(cfg)
+    geo = geometry_of(cfg)
+    rank_of = np.array([0, 0, 1, 1, 2, 2], dtype=np.int32)
+    r = torch.from_numpy(rank_of).to("cuda:0")
+    mask, counts, kv, extra = fva.fva_route_sasa(to_dev(Qb), to_dev(Kb), cfg.p, cfg.k_min, tiling_of(cfg), r, 3, 0.8, 0.0)
+    torch.cuda.synchronize()
+    order = np.concatenate([route_ref(f64(Qb[b]), f64(Kb[b]), cfg.p, cfg.k_min, geo)["order"] for b in range(2)])
+    c0 = np.concatenate([route_ref(f64(Qb[b]), f64(Kb[b]), cfg.p, cfg.k_min, geo)["counts"] for b in range(2)])
+    m_ref, c_ref, e_ref, _ = sasa_augment(order, c0, rank_of, 3, 0.8, 0.0)
+    assert np.array_equal(extra.cpu().numpy(), e_ref)
+    assert np.array_equal(counts.cpu().numpy().reshape(6, -1), c_ref)
+    assert np.array_equal(mask.cpu().numpy().reshape(6, geo.nb, geo.nb), m_ref)
+    log(f"[sasa] batch 2: extra per rank {e_ref.tolist()}")
