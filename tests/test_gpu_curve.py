@@ -135,7 +135,7 @@ def test_curve_route_attn_tiny():
     assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
 
 
-@pytest.mark.parametrize("name", ["480p", "720p"])
+@pytest.mark.parametrize("name", ["480p", "720p", "720p_stress", "long"])
 def test_curve_route_attn_full_workloads(name):
     cfg = synth.get_config(name)
     Qb, Kb, Vb = workload(name)

@@ -157,7 +157,7 @@ def test_fp8_attn_host_masks_partial_blocks(kind, grid, tile):
     compare_rows(f"{grid} {kind}", Qb, Kb, Vb, m[0], O[0], geo, {h: list(range(geo.nb)) for h in range(3)})
 
 
-@pytest.mark.parametrize("name", ["480p", "720p"])
+@pytest.mark.parametrize("name", ["480p", "720p", "720p_stress", "long"])
 def test_fp8_attn_full_workloads_sampled(name):
     fva = lib()
     cfg = synth.get_config(name)
