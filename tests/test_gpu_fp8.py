@@ -228,3 +228,17 @@ def test_fp8_attn_batch_two_odd_heads():
         sel = lambda X: X[b:b + 1]
         compare_rows(f"batch {b}", sel(Qb), sel(Kb), sel(Vb), mask.cpu().numpy()[b], O[b], geo,
                      {h: list(range(geo.nb)) for h in range(3)})
+
+
+def test_fp8_attn_max_blocks_sampled():
+    # nb = 1024, the largest supported block count (16 x 128 x 64 tokens, 2x8x8 boxes)
+    fva, torch = lib(), torch_mod()
+    cfg = custom_config("fp8max", 1, (16, 128, 64), (2, 8, 8), (1.5,), seed=11)
+    geo = geometry_of(cfg)
+    assert geo.nb == 1024
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    t = tiling_of(cfg)
+    mask, counts, kv = fva.fva_route(to_dev(Qb), to_dev(Kb), cfg.p, cfg.k_min, t)
+    O = fp8_attn(Qb, Kb, Vb, t, mask, counts, kv)
+    rows = {0: [0, 511, 777, 1023]}
+    compare_rows("max blocks", Qb, Kb, Vb, mask.cpu().numpy()[0], O[0], geo, rows)

@@ -109,3 +109,12 @@ def test_sasa_batch_two():
     assert np.array_equal(counts.cpu().numpy().reshape(6, -1), c_ref)
     assert np.array_equal(mask.cpu().numpy().reshape(6, geo.nb, geo.nb), m_ref)
     log(f"[sasa] batch 2: extra per rank {e_ref.tolist()}")
+
+
+def test_sasa_one_rank_per_head_and_max_ranks():
+    cfg = synth.get_config("480p")
+    Qb, Kb, _ = workload("480p")
+    check("480p, 40 ranks", Qb, Kb, cfg, np.arange(cfg.heads), cfg.heads)
+    # 1024 ranks, heads spread over a few of them, the rest empty
+    rank_of = (np.arange(cfg.heads) % 4) * 255
+    check("480p, 1024 ranks", Qb, Kb, cfg, rank_of, 1024)
