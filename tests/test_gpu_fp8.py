@@ -157,6 +157,30 @@ def test_fp8_attn_host_masks_partial_blocks(kind, grid, tile):
     compare_rows(f"{grid} {kind}", Qb, Kb, Vb, m[0], O[0], geo, {h: list(range(geo.nb)) for h in range(3)})
 
 
+@pytest.mark.parametrize("s", [1, 3])
+def test_fp8_attn_empty_rows_and_forced_splits(s):
+    # Partial blocks (21 = 2*10 + 1 frames, 13 = 8 + 5 rows) with every third
+    # query block keeping nothing: those rows must be exactly zero, whole rows
+    # and rows cut into chunks of s kept blocks (combined from partials) must
+    # meet the same bar against the oracle.
+    fva = lib()
+    cfg = custom_config("fp8split", 3, (5, 13, 21), (2, 8, 8), (0.3, 1.5, 5.0), seed=29)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    geo = geometry_of(cfg)
+    rng = np.random.default_rng(31)
+    m = (rng.random((1, 3, geo.nb, geo.nb)) < 0.6).astype(np.uint8)
+    empty = list(range(0, geo.nb, 3))
+    m[0, :, empty, :] = 0
+    mt = torch_mod().from_numpy(m).to("cuda:0")
+    kept = {h: [i for i in range(geo.nb) if i not in empty] for h in range(3)}
+    for flags, name in [(0, "whole rows"), (fva.FVA_SPLIT_BLOCKS(s), f"chunks of {s}")]:
+        O = fp8_attn(Qb, Kb, Vb, tiling_of(cfg), mt, flags=flags)
+        for h in range(3):
+            for i in empty:
+                assert np.all(O[0, h][geo.block_tokens[i]] == 0), (name, h, i)
+        compare_rows(f"empty rows, {name}", Qb, Kb, Vb, m[0], O[0], geo, kept)
+
+
 @pytest.mark.parametrize("name", ["480p", "720p", "720p_stress", "long"])
 def test_fp8_attn_full_workloads_sampled(name):
     fva = lib()
