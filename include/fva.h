@@ -35,8 +35,9 @@
  *   and outputs are distinct.
  * - Supported shapes: head_dim == 128, bt*bh*bw in {64, 128}, nb <= 1024,
  *   tokens * stride_n * 2 < 2^31 (one head addressed with 32-bit byte
- *   offsets). Anything else returns FVA_ERR_UNSUPPORTED (there is no slow
- *   generic path).
+ *   offsets), and batch * heads <= 65535 for the routing calls,
+ *   fva_quantize_v and fva_permute_tokens. Anything else returns
+ *   FVA_ERR_UNSUPPORTED (there is no slow generic path).
  */
 #ifndef FVA_H
 #define FVA_H
@@ -53,7 +54,7 @@ typedef enum fva_status {
   FVA_ERR_INVALID_ARG = -1, /* null pointer, p outside [0,1] or NaN, k_min < 0, bad flags */
   FVA_ERR_SHAPE = -2,       /* tokens != T*H*W, non-positive extents, bad strides */
   FVA_ERR_UNSUPPORTED = -3, /* head_dim != 128, tile volume not 64/128, nb > 1024, head > 2 GiB,
-                               curve grid extent > 256 */
+                               curve grid extent > 256, batch*heads > 65535 where noted */
   FVA_ERR_WORKSPACE = -4,   /* workspace missing or smaller than the query says */
   FVA_ERR_HIP = -5          /* a kernel launch failed */
 } fva_status;
@@ -115,6 +116,8 @@ fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* 
  *          entries; later entries are left untouched.
  * workspace: at least fva_route_workspace_size bytes of device memory,
  *          256-byte aligned.
+ * Errors : as in the conventions above; FVA_ERR_UNSUPPORTED also for
+ *          batch * heads > 65535.
  */
 fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, double p, int32_t k_min,
                      const fva_tiling* tiling, uint8_t* block_mask, int32_t* counts, int32_t* kv_idx,

@@ -100,6 +100,7 @@ fva_status route_common(const void* Q, const void* K, const fva_qkv_desc* desc, 
   const fva_status s = check_shape(desc, tiling, &nb);
   if (s != FVA_OK) return s;
   if (!aligned16(Q) || !aligned16(K)) return FVA_ERR_INVALID_ARG;
+  if ((int64_t)desc->batch * desc->heads > 65535) return FVA_ERR_UNSUPPORTED;  // pool grid's y extent
   const size_t need = rank_of ? fva::route_sasa_workspace_bytes(desc->batch, desc->heads, nb)
                               : fva::route_workspace_bytes(desc->batch, desc->heads, nb);
   if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;

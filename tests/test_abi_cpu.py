@@ -112,6 +112,7 @@ def test_route_argument_errors():
     bad = desc()
     bad.stride_n = 100  # rows overlap and are not 16-byte aligned
     assert _route(d=bad) == fva.FVA_ERR_SHAPE
+    assert _route(d=desc(B=2, H=40000)) == fva.FVA_ERR_UNSUPPORTED  # more than 65535 heads in all
 
 
 def _attn(flags=0, counts=None, kv=None, mask=FAKE, trace=None, scale=0.0, ws=FAKE, wsb=1 << 40, o=FAKE):
