@@ -259,6 +259,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true", help="skip the scheduler imbalance trace runs")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--flushed-reps", type=int, default=20,
+                    help="steps timed one by one after a 512 MB cache-flushing write, outside the timed region (0: skip)")
     ap.add_argument("--copy-calibration", action="store_true", help="only time a 1 GiB device copy")
     args = ap.parse_args()
 
@@ -372,6 +374,32 @@ def main():
 
     ms_per_step, t_route, t_attn = timed(p, args.steps, args.warmup)
     t_quant = timed.quant_s
+
+    def flushed(pp, reps, warmup=3, flush_mb=512):
+        # Each step timed alone after writing a 512 MB buffer (larger than the
+        # 256 MB Infinity Cache), on the same stream; median and min.
+        scratch = torch.empty(flush_mb << 20, dtype=torch.uint8, device=dev)
+        for _ in range(warmup):
+            step(pp)
+        rows = []
+        for _ in range(reps):
+            scratch.fill_(1)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            step(pp, ev)
+            torch.cuda.synchronize()
+            rows.append((ev[0].elapsed_time(ev[2]), ev[3].elapsed_time(ev[1]) * 1e3, ev[1].elapsed_time(ev[2])))
+        del scratch
+        a = np.array(rows)
+        med, mn = np.median(a, axis=0), a.min(axis=0)
+        return {"reps": reps, "warmup": warmup, "flush_MB": flush_mb,
+                "step_ms_median": round(float(med[0]), 4), "step_ms_min": round(float(mn[0]), 4),
+                "route_us_median": round(float(med[1]), 2), "route_us_min": round(float(mn[1]), 2),
+                "attn_ms_median": round(float(med[2]), 4), "attn_ms_min": round(float(mn[2]), 4)}
+
+    flushed_res = flushed(p, args.flushed_reps) if args.flushed_reps > 0 else None
+    if flushed_res:
+        log(f"[bench] {args.flushed_reps} steps after a cache flush each: median {flushed_res['step_ms_median']:.3f} ms, "
+            f"min {flushed_res['step_ms_min']:.3f} ms")
     log(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step (route {t_route*1e6:.1f} us, "
         f"attn {t_attn*1e3:.3f} ms" + (f", V quantisation {t_quant*1e6:.1f} us)" if fp8 else ")"))
 
@@ -461,6 +489,8 @@ def main():
             "attn_source_digest": digest,
         },
     }
+    if flushed_res:
+        res["flushed_steps"] = flushed_res
     if curve is not None:
         res["curve_layout"] = curve
     if args.sasa:
