@@ -259,6 +259,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true", help="skip the scheduler imbalance trace runs")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--dense-reps", type=int, default=3,
+                    help="runs of the same attention with every block kept (dense comparator), outside the timed region")
     ap.add_argument("--flushed-reps", type=int, default=20,
                     help="steps timed one by one after a 512 MB cache-flushing write, outside the timed region (0: skip)")
     ap.add_argument("--copy-calibration", action="store_true", help="only time a 1 GiB device copy")
@@ -396,6 +398,42 @@ def main():
                 "route_us_median": round(float(med[1]), 2), "route_us_min": round(float(mn[1]), 2),
                 "attn_ms_median": round(float(med[2]), 4), "attn_ms_min": round(float(mn[2]), 4)}
 
+    def dense(reps):
+        # The same attention call with every key block kept for every query
+        # block (counts = nb, kept lists 0 .. nb-1): the dense work the
+        # routing avoids, on the same kernel.
+        ones = torch.ones_like(mask)
+        c_all = torch.full_like(counts, nb)
+        kv_all = torch.arange(nb, dtype=torch.int32, device=dev).expand(B, H, nb, nb).contiguous()
+        o_d = torch.empty_like(out)
+
+        def run():
+            if fp8:
+                fva.fva_attn_fp8v(q, k, v8, vexp, tiling, ones, c_all, kv_all, flags=flags, out=o_d, workspace=ws_a)
+            else:
+                fva.fva_attn(q, k, v, tiling, ones, c_all, kv_all, flags=flags, out=o_d, workspace=ws_a)
+
+        run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps / 1e3
+        all_flops = 4.0 * 128 * 128 * 128 * B * H * nb * nb
+        del ones, c_all, kv_all, o_d
+        return t, all_flops
+
+    dense_res = None
+    if args.dense_reps > 0:
+        t_dense, dense_tile_flops = dense(args.dense_reps)
+        dense_res = {"reps": args.dense_reps, "attn_ms": round(t_dense * 1e3, 3),
+                     "kept_tile_TFLOPS": round(dense_tile_flops / t_dense / 1e12, 1),
+                     "useful_TFLOPS": round(4.0 * B * H * float(cfg.N) ** 2 * 128 / t_dense / 1e12, 1)}
+        log(f"[bench] dense comparator (every block kept): {t_dense * 1e3:.2f} ms")
+
     flushed_res = flushed(p, args.flushed_reps) if args.flushed_reps > 0 else None
     if flushed_res:
         log(f"[bench] {args.flushed_reps} steps after a cache flush each: median {flushed_res['step_ms_median']:.3f} ms, "
@@ -489,6 +527,10 @@ def main():
             "attn_source_digest": digest,
         },
     }
+    if dense_res:
+        dense_res["speedup_attn"] = round(dense_res["attn_ms"] / (t_attn * 1e3), 3)
+        dense_res["speedup_step"] = round(dense_res["attn_ms"] / ms_per_step, 3)
+        res["dense_comparator"] = dense_res
     if flushed_res:
         res["flushed_steps"] = flushed_res
     if curve is not None:
