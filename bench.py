@@ -259,6 +259,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true", help="skip the scheduler imbalance trace runs")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--reverse-heads", action="store_true",
+                    help="reverse the head order of Q, K, V (scheduler diagnostic: the head-major grid's tail changes)")
     ap.add_argument("--dense-reps", type=int, default=3,
                     help="runs of the same attention with every block kept (dense comparator), outside the timed region")
     ap.add_argument("--flushed-reps", type=int, default=20,
@@ -289,6 +291,9 @@ def main():
     log(f"[bench] generating {cfg.name}: {cfg.heads} heads x {cfg.N} tokens x 128")
     Qb, Kb, Vb = synth.gen_qkv(cfg)
     up = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+    if args.reverse_heads:
+        Qb, Kb, Vb = (np.ascontiguousarray(a[:, ::-1]) for a in (Qb, Kb, Vb))
+        log("[bench] head order reversed")
     q, k, v = up(Qb), up(Kb), up(Vb)
     curve = None
     if args.blocks == "hilbert":
@@ -491,6 +496,7 @@ def main():
             "p": p,
             "k_min": cfg.k_min,
             "scheduler": args.sched,
+            **({"head_order": "reversed"} if args.reverse_heads else {}),
             "parallelism": "single GPU",
         },
         "attn_ms": round(t_attn * 1e3, 4),
