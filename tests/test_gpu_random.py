@@ -9,7 +9,11 @@ to 1 and k_min from 0 to 6. For each case:
 * the mask by the routing rule (bit-exact except band and tie blocks,
   oracle/compare.py), counts = row sums and ascending kept lists;
 * the attention output on the GPU's own mask, every element, within
-  max 2e-2 / mean 1e-3 of the fp64 oracle.
+  max 2e-2 / mean 1e-3 of the fp64 oracle;
+* the same with E4M3 V (the bar of tests/test_gpu_fp8.py: the oracle on the
+  dequantised V, P-rounding bound plus 2e-2), empty rows exactly zero;
+* the same with Hilbert-curve blocks of the box volume (the checks of
+  tests/test_gpu_curve.py, batch 0).
 """
 
 import numpy as np
@@ -72,4 +76,57 @@ def test_random_small_config(case):
     log(f"[random {case}] grid {cfg.grid} tile {cfg.tile} batch {cfg.batch} heads {cfg.heads} p {cfg.p} "
         f"k_min {cfg.k_min}: nb {nb}, retained {c.mean() / nb:.3f}, band {band} tie {tie}, "
         f"attn max {e.max():.2e} mean {e.mean():.2e}")
+    assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
+
+
+@pytest.mark.parametrize("case", range(30))
+def test_random_small_config_fp8v(case):
+    # The same configurations with E4M3 V: the quantiser's exponents and the
+    # attention against the oracle on the dequantised V, within the
+    # P-rounding bound plus the bf16 bar (tests/test_gpu_fp8.py).
+    from test_gpu_fp8 import compare_rows
+
+    fva, torch = lib(), torch_mod()
+    cfg = draw(case)
+    geo = geometry_of(cfg)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    q, k, v = to_dev(Qb), to_dev(Kb), to_dev(Vb)
+    tiling = tiling_of(cfg)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling)
+    v8, vexp = fva.fva_quantize_v(v, tiling)
+    out = fva.fva_attn_fp8v(q, k, v8, vexp, tiling, mask, counts, kv)
+    torch.cuda.synchronize()
+    m = mask.cpu().numpy()
+    O = out.float().cpu().numpy().astype(np.float64)
+    rows = {h: list(range(geo.nb)) for h in range(cfg.heads)}
+    for b in range(cfg.batch):
+        compare_rows(f"random {case} batch {b}", Qb[b:b + 1], Kb[b:b + 1], Vb[b:b + 1], m[b], O[b], geo, rows)
+        for h in range(cfg.heads):
+            for i in range(geo.nb):
+                if not m[b, h, i].any():
+                    assert np.all(O[b, h][geo.block_tokens[i]] == 0)
+
+
+@pytest.mark.parametrize("case", range(30))
+def test_random_small_config_curve(case):
+    # The same configurations with Hilbert-curve blocks of the box volume:
+    # tokens permuted along the curve, routed and attended with the
+    # one-dimensional tiling, O permuted back; checked against the oracle run
+    # with curve blocks on the raster inputs (batch 0).
+    from test_gpu_curve import check_mask, curve_run
+
+    from oracle import curve_geometry
+
+    cfg = draw(case)
+    B = int(np.prod(cfg.tile))
+    geo = curve_geometry(*cfg.grid, B)
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    mask, counts, kv, O = curve_run(Qb, Kb, Vb, cfg.grid, B, cfg.p, cfg.k_min)
+    check_mask(f"random {case}", mask, counts, kv, Qb, Kb, geo, cfg.p, cfg.k_min)
+    errs = []
+    for h in range(cfg.heads):
+        ref = attn_ref_head(f64(Qb[0, h]), f64(Kb[0, h]), f64(Vb[0, h]), mask[0, h], geo)
+        errs.append(np.abs(O[h] - ref).ravel())
+    e = np.concatenate(errs)
+    log(f"[random curve {case}] nb {geo.nb}: attn max {e.max():.2e} mean {e.mean():.2e}")
     assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
