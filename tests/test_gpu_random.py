@@ -13,7 +13,9 @@ to 1 and k_min from 0 to 6. For each case:
 * the same with E4M3 V (the bar of tests/test_gpu_fp8.py: the oracle on the
   dequantised V, P-rounding bound plus 2e-2), empty rows exactly zero;
 * the same with Hilbert-curve blocks of the box volume (the checks of
-  tests/test_gpu_curve.py, batch 0).
+  tests/test_gpu_curve.py, batch 0);
+* routing with slack-aware augmentation over a random head -> rank map,
+  bit-exact (tests/test_gpu_sasa.py).
 """
 
 import numpy as np
@@ -130,3 +132,23 @@ def test_random_small_config_curve(case):
     e = np.concatenate(errs)
     log(f"[random curve {case}] nb {geo.nb}: attn max {e.max():.2e} mean {e.mean():.2e}")
     assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
+
+
+@pytest.mark.parametrize("case", range(30))
+def test_random_small_config_sasa(case):
+    # The same configurations (batch 1) routed with slack-aware augmentation
+    # over a random head -> rank map (ids outside [0, n_ranks) take no part)
+    # and random n1, n2: mask, counts, kept lists and per-rank extra blocks
+    # bit-exact against the oracle (tests/test_gpu_sasa.py).
+    import dataclasses
+
+    from test_gpu_sasa import check
+
+    cfg = dataclasses.replace(draw(case), batch=1)
+    rng = np.random.default_rng([4048, case])
+    n_ranks = int(rng.integers(1, 5))
+    rank_of = rng.integers(-1, n_ranks + 1, size=cfg.heads).astype(np.int32)
+    n1 = float(rng.choice([0.0, 0.5, 0.8, 1.0]))
+    n2 = float(rng.choice([0.0, 0.07, 0.3]))
+    Qb, Kb, _ = synth.gen_qkv(cfg)
+    check(f"random {case}", Qb, Kb, cfg, rank_of, n_ranks, n1=n1, n2=n2)
