@@ -231,3 +231,21 @@ def test_status_strings():
     for s in (-1, -2, -3, -4, -5):
         assert fva.fva_status_string(s) != "unknown status"
     assert fva.fva_status_string(7) == "unknown status"
+
+
+def test_host_tensors_are_refused_no_cpu_fallback():
+    # Every compute entry point takes device tensors only: host tensors are an
+    # error, never a slower path.
+    import torch
+
+    t = fva.Tiling(3, 16, 16, 1, 8, 8)
+    q = torch.zeros(1, 2, 3 * 16 * 16, 128, dtype=torch.bfloat16)
+    mask = torch.ones(1, 2, 12, 12, dtype=torch.uint8)
+    with pytest.raises(ValueError):
+        fva.fva_route(q, q, 0.9, 2, t)
+    with pytest.raises(ValueError):
+        fva.fva_attn(q, q, q, t, mask)
+    with pytest.raises(ValueError):
+        fva.fva_quantize_v(q, t)
+    with pytest.raises(ValueError):
+        fva.fva_route_sasa(q, q, 0.9, 2, t, torch.zeros(2, dtype=torch.int32), 2, 0.8, 0.07)
