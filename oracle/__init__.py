@@ -13,8 +13,8 @@ Balancing for Video Generation"):
   (routing frontend paragraph), as 3D boxes or as runs of a Hilbert curve
   (the block reordering of the same paragraph);
 * block mask M_{h,i,j} over (query block, key block) pairs -- §2.1;
-* Top-p: the smallest set of key blocks whose cumulative normalised
-  importance reaches p -- §2.1;
+* Top-p: keep key blocks in decreasing score order until their summed
+  softmax mass is at least p (m_p = min{r : c_r >= p}) -- §2.1;
 * Top-k safety floor -- §2.1 and §3.1;
 * realised per-head workload L_h = mean_i sum_j M_{h,i,j} -- §2.2, Eq. 1;
 * block-sparse attention over the retained blocks only -- §2.1, §3.1;

@@ -13,8 +13,8 @@ not name the format. The reading taken here:
   and the scaling itself is exact; the quantised V is 2^e_d * E4M3(V * 2^-e_d);
 * attention then runs on the dequantised V with the same mask
   (attention.py); the probabilities P are also rounded to E4M3 inside the
-  GPU kernel, which the oracle does not model (their effect is bounded in
-  the tests instead).
+  GPU kernel, which the oracle does not model: p_rounding_bound bounds their
+  effect, normal range, subnormals and flush to zero included.
 
 Written from the format definition with numpy; nothing is shared with the
 GPU library.
@@ -95,18 +95,64 @@ def dequantize_v(codes: np.ndarray, e: np.ndarray) -> np.ndarray:
     return np.ldexp(e4m3_decode(codes), np.asarray(e)[None, :])
 
 
-def p_rounding_bound(Q, K, Vq, mask, geo, rows, scale=None, u=2.0**-4):
-    """Per-element bounds on the effect of rounding P to E4M3 (relative error <= u).
+# The GPU kernel rounds every probability as v = x * 2^(7 + delta) to E4M3,
+# x = exp(s - s_max) being the probability relative to the row's maximum and
+# delta >= 0 the distance (in powers of two) from the row's maximum down to the
+# exponent reference the kernel held when it rounded that key (the reference
+# never exceeds the running maximum). Hence, in units of x:
+#   * x >= 2^-13 (v >= 2^-6, the smallest normal): |dx| <= u x (3-bit
+#     mantissa, round to nearest: u = 2^-4);
+#   * x < 2^-13 (v possibly subnormal, spacing 2^-9): |dv| <= min(v, 2^-10)
+#     -- half a quantum, and values below half the smallest subnormal flush
+#     to zero (|dv| = v) -- so |dx| <= min(x, 2^-17 * 2^-delta) <= min(x, 2^-17).
+# Both cases together: |dx| <= c(x) x with c(x) = max(u, min(1, 2^-17 / x)),
+# continuous in x (u at x = 2^-13, 1 at x = 2^-17), whatever delta >= 0 is, so
+# the bound needs the row maximum only and not the kernel's reference.
+P_PRESCALE_LOG2 = 7
 
-    For each query block i in `rows` returns (bound, rms), both (n_i x d):
-    with w_k the exact softmax weights of the row and O' the exact output on
-    the dequantised V, a relative error eps_k (|eps_k| <= u) on every P_k
-    changes the normalised output by sum_k w_k eps_k (v_k - O') / (1 + sum_k
-    w_k eps_k), so
-        bound = u / (1 - u) * sum_k w_k |v_k - O'|,
-        rms   = u * sqrt(sum_k w_k^2 (v_k - O')^2)   (the size of the sum for
-                independent errors of spread u).
+
+def p_rounding_factors(x, u=2.0**-4, prescale_log2=P_PRESCALE_LOG2):
+    """c(x): bound on |dx| / x for probabilities x <= 1 relative to the row maximum.
+
+    x is rounded to E4M3 as x * 2^(prescale + delta) for any delta >= 0; the
+    normal range starts at x = 2^(-6 - prescale), half a subnormal quantum is
+    2^(-10 - prescale) in units of x.
     """
+    x = np.asarray(x, dtype=np.float64)
+    half_quantum = 2.0 ** (-10 - prescale_log2)
+    with np.errstate(divide="ignore"):
+        sub = np.where(x > 0, np.minimum(1.0, half_quantum / np.where(x > 0, x, 1.0)), 1.0)
+    return np.maximum(u, sub)
+
+
+def p_rounding_bound(Q, K, Vq, mask, geo, rows, scale=None, u=2.0**-4, prescale_log2=P_PRESCALE_LOG2,
+                     method="exact", with_output=False, heavy_w=1e-3):
+    """Per-element bounds on the effect of rounding P to E4M3.
+
+    For each query block i in `rows` returns (bound, rms), both (n_i x d), or
+    (O', bound, rms) with with_output. With x_k = exp(s_k - s_max) over the
+    row's kept keys, Z = sum_k x_k, w_k = x_k / Z the exact softmax weights,
+    O' = sum_k w_k v_k the exact output on the dequantised V, and the rounded
+    x_k + e_k with |e_k| <= c_k x_k (c_k = p_rounding_factors(x_k)): the
+    kernel's normalised output is sum_k (x_k + e_k) v_k / sum_k (x_k + e_k),
+    and since sum_k x_k (v_k - O') = 0,
+        O - O' = sum_k e_k (v_k - O') / (Z + sum_k e_k),
+    so, with beta = sum_k c_k w_k < 1 and d_k = v_k - O',
+        exact:   bound = sum_k c_k w_k |d_k| / (1 - beta)   (exact, not first order),
+        cauchy:  the same sum taken exactly over the row's heavy keys
+                 (w_k > heavy_w, at most 1 / heavy_w of them) and bounded by
+                 Cauchy-Schwarz over the rest, sqrt(sum' c_k w_k) *
+                 sqrt(sum' c_k w_k d_k^2), divided by (1 - beta): never below
+                 the exact bound (up to fp64 cancellation in the expanded
+                 squares, below 1e-7 absolute), and the light part is matrix
+                 products only (for large row sets, where the exact sum costs
+                 rows x keys x d),
+        rms      = sqrt(sum_k (c_k w_k)^2 d_k^2)   (the size of the sum for
+                 independent errors of that spread).
+    A row with beta >= 1 gets an infinite bound (nothing is claimed for it).
+    """
+    if method not in ("exact", "cauchy"):
+        raise ValueError("method is 'exact' or 'cauchy'")
     Q = np.asarray(Q, dtype=np.float64)
     K = np.asarray(K, dtype=np.float64)
     Vq = np.asarray(Vq, dtype=np.float64)
@@ -117,20 +163,45 @@ def p_rounding_bound(Q, K, Vq, mask, geo, rows, scale=None, u=2.0**-4):
         qi = geo.block_tokens[i]
         kept = np.nonzero(mask[i])[0]
         if kept.size == 0:
-            z = np.zeros((len(qi), d))
-            out[int(i)] = (z, z)
+            z = np.zeros((len(qi), Vq.shape[1]))
+            out[int(i)] = (z, z, z) if with_output else (z, z)
             continue
         keys = np.concatenate([geo.block_tokens[j] for j in kept])
         S = tau * (Q[qi] @ K[keys].T)
-        S -= S.max(axis=1, keepdims=True)
-        Wt = np.exp(S)
-        Wt /= Wt.sum(axis=1, keepdims=True)
-        O = Wt @ Vq[keys]
-        bound = np.empty_like(O)
-        rms = np.empty_like(O)
-        for c in range(d):
-            dev = Vq[keys, c][None, :] - O[:, c][:, None]
-            bound[:, c] = (Wt * np.abs(dev)).sum(axis=1)
-            rms[:, c] = np.sqrt((Wt * Wt * dev * dev).sum(axis=1))
-        out[int(i)] = (bound * u / (1.0 - u), rms * u)
+        X = np.exp(S - S.max(axis=1, keepdims=True))
+        Wt = X / X.sum(axis=1, keepdims=True)
+        Vk = Vq[keys]
+        O = Wt @ Vk
+        CW = p_rounding_factors(X, u, prescale_log2) * Wt
+        beta = CW.sum(axis=1)
+        denom = np.where(beta < 1.0, 1.0 - beta, 0.0)
+        if method == "exact":
+            num = np.empty_like(O)
+            ms = np.empty_like(O)
+            for c in range(Vq.shape[1]):
+                dev = Vk[:, c][None, :] - O[:, c][:, None]
+                num[:, c] = (CW * np.abs(dev)).sum(axis=1)
+                ms[:, c] = (CW * CW * dev * dev).sum(axis=1)
+        else:
+            # heavy keys exactly: one term per (query row, heavy key) pair
+            heavy = Wt > heavy_w
+            qh, kh = np.nonzero(heavy)  # row-major: pairs of one row are consecutive
+            num = np.zeros_like(O)
+            if qh.size:
+                terms = CW[qh, kh][:, None] * np.abs(Vk[kh] - O[qh])
+                starts = np.flatnonzero(np.r_[True, qh[1:] != qh[:-1]])
+                num[qh[starts]] = np.add.reduceat(terms, starts, axis=0)
+            # light keys by Cauchy-Schwarz, with
+            # sum_k a_k (v_k - o)^2 = (a @ v^2) - 2 o (a @ v) + o^2 sum_k a_k
+            V2 = Vk * Vk
+            CL = np.where(heavy, 0.0, CW)
+            bl = CL.sum(axis=1)
+            var = CL @ V2 - 2.0 * O * (CL @ Vk) + O * O * bl[:, None]
+            num += np.sqrt(bl[:, None] * np.maximum(var, 0.0))
+            CW2 = CW * CW
+            ms = CW2 @ V2 - 2.0 * O * (CW2 @ Vk) + O * O * CW2.sum(axis=1)[:, None]
+        with np.errstate(divide="ignore", invalid="ignore"):
+            bound = np.where(denom[:, None] > 0, num / np.where(denom > 0, denom, 1.0)[:, None], np.inf)
+        rms = np.sqrt(np.maximum(ms, 0.0))
+        out[int(i)] = (O, bound, rms) if with_output else (bound, rms)
     return out

@@ -8,8 +8,8 @@ Follows, in the paper's order:
    reading taken here, the usual attention scale);
 2. normalised importance (§2.1): P_ij = softmax_j(s_ij) over all key blocks of
    the row;
-3. Top-p (§2.1): the smallest set of key blocks whose cumulative normalised
-   importance reaches p. The blocks are taken in decreasing score order (ties
+3. Top-p (§2.1): keep key blocks in decreasing score order until their
+   summed softmax mass is at least p. The blocks are taken in that order (ties
    to the lower block id), c_r is the running sum of their P, and
    m_p = min{r : c_r >= p}, or nb when no prefix reaches p; p = 1 keeps all
    blocks, as it does in exact arithmetic;

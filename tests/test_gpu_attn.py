@@ -16,7 +16,20 @@ import synth
 from oracle import attn_ref_head, attn_ref_rows
 from oracle.compare import ATTN_MAX_ABS, ATTN_MEAN_ABS, attn_errors
 
-from _gpu_util import custom_config, f64, geometry_of, lib, log, tiling_of, to_dev, torch_mod, workload
+from _gpu_util import (
+    attn_rule_errors,
+    custom_config,
+    describe_rows,
+    f64,
+    geometry_of,
+    lib,
+    log,
+    rule_rows,
+    tiling_of,
+    to_dev,
+    torch_mod,
+    workload,
+)
 
 pytestmark = pytest.mark.gpu
 
@@ -127,47 +140,44 @@ def test_attn_custom_scale_and_strided_layout():
     compare_full("strided scale=0.05", Qb, Kb, Vb, cfg, mask, o64(O), scale=0.05)
 
 
-def sampled_rows(counts, nb, rng, n_random=32, per_head=8):
-    """(h, i) pairs: 4 heads (min, max density, two random) x per_head rows, plus random rows."""
-    dens = counts.mean(axis=-1)
-    H = counts.shape[0]
-    heads = [int(np.argmin(dens)), int(np.argmax(dens))]
-    heads += [int(h) for h in rng.choice([h for h in range(H) if h not in heads], 2, replace=False)]
-    pairs = set()
-    for h in heads:
-        for i in rng.choice(nb, per_head, replace=False):
-            pairs.add((h, int(i)))
-    while len(pairs) < len(heads) * per_head + n_random:
-        pairs.add((int(rng.integers(H)), int(rng.integers(nb))))
-    return sorted(pairs)
-
-
-@pytest.mark.parametrize("name", ["480p", "720p", "720p_stress", "long"])
-def test_attn_full_workloads_sampled(name):
+def check_full(name, cfg, p, all_heads=False, seed=31):
+    """Route and attend at full size in the benchmark's launch configuration
+    (persistent scheduler, kept lists from fva_route), then compare the
+    query blocks of rule_rows (all heads with all_heads) with the oracle."""
     fva = lib()
-    cfg = synth.get_config(name)
     geo = geometry_of(cfg)
-    Qb, Kb, Vb = workload(name)
+    Qb, Kb, Vb = workload(cfg.name)
     q, k, v = upload(Qb, Kb, Vb)
-    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    mask, counts, kv = fva.fva_route(q, k, p, cfg.k_min, tiling_of(cfg))
     O = run_attn(q, k, v, cfg, mask, counts, kv)
     m = mask.cpu().numpy()[0]
     c = counts.cpu().numpy()[0]
-    rng = np.random.default_rng(31)
-    pairs = sampled_rows(c, geo.nb, rng)
     Of = O[0].float().cpu().numpy()
-    errs = []
-    by_head = {}
-    for h, i in pairs:
-        by_head.setdefault(h, []).append(i)
-    for h, rows in by_head.items():
-        ref = attn_ref_rows(f64(Qb[0, h]), f64(Kb[0, h]), f64(Vb[0, h]), m[h], geo, rows)
-        for i, o in ref.items():
-            errs.append(np.abs(Of[h][geo.block_tokens[i]] - o).ravel())
-    e = np.concatenate(errs)
-    log(f"[attn] {name}: {len(pairs)} sampled rows, max abs {e.max():.3e} mean abs {e.mean():.3e}, "
-        f"density {c.mean() / geo.nb:.3f}")
-    assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
+    del q, k, v, O
+    rows = rule_rows(c, geo.nb, seed, all_heads=all_heads)
+    emax, emean, n = attn_rule_errors(Qb, Kb, Vb, m, Of, geo, rows)
+    log(f"[attn] {name} p={p}: {describe_rows(rows)}, {n} elements compared, max abs {emax:.3e} "
+        f"mean abs {emean:.3e}, density {c.mean() / geo.nb:.3f}")
+    assert emax <= ATTN_MAX_ABS and emean <= ATTN_MEAN_ABS
+
+
+@pytest.mark.parametrize("name", ["720p", "720p_stress", "long"])
+def test_attn_full_workloads_rule(name):
+    # every query block of the lowest- and highest-density heads and of two
+    # random heads, plus 64 random (head, block) rows
+    cfg = synth.get_config(name)
+    check_full(name, cfg, cfg.p)
+
+
+def test_attn_480p_all_heads():
+    cfg = synth.get_config("480p")
+    check_full("480p", cfg, cfg.p, all_heads=True)
+
+
+@pytest.mark.parametrize("p", [0.8, 0.95])
+def test_attn_long_p_sweep_rule(p):
+    cfg = synth.get_config("long")
+    check_full("long", cfg, p, seed=int(p * 100))
 
 
 def test_attn_deterministic_and_trace():

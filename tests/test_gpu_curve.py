@@ -17,7 +17,7 @@ import synth
 from oracle import attn_ref_head, attn_ref_rows, curve_geometry, curve_order, route_ref
 from oracle.compare import ATTN_MAX_ABS, ATTN_MEAN_ABS, compare_mask_rows
 
-from _gpu_util import f64, lib, log, to_dev, torch_mod, workload
+from _gpu_util import attn_rule_errors, describe_rows, f64, lib, log, rule_rows, to_dev, torch_mod, workload
 
 pytestmark = pytest.mark.gpu
 
@@ -137,24 +137,18 @@ def test_curve_route_attn_tiny():
 
 @pytest.mark.parametrize("name", ["480p", "720p", "720p_stress", "long"])
 def test_curve_route_attn_full_workloads(name):
+    # masks of every head against the oracle; attention on every query block
+    # of the lowest- and highest-density heads and of two random heads (the
+    # partial last block included), plus 64 random (head, block) rows
     cfg = synth.get_config(name)
     Qb, Kb, Vb = workload(name)
     geo = curve_geometry(*cfg.grid, 128)
     mask, counts, kv, O = curve_run(Qb, Kb, Vb, cfg.grid, 128, cfg.p, cfg.k_min)
     check_mask(name, mask, counts, kv, Qb, Kb, geo, cfg.p, cfg.k_min)
-    c = counts[0]
-    dens = c.mean(axis=-1)
-    rng = np.random.default_rng(17)
-    heads = [int(np.argmin(dens)), int(np.argmax(dens)), int(rng.integers(cfg.heads))]
-    errs = []
-    for h in heads:
-        rows = sorted({int(i) for i in rng.choice(geo.nb, 6, replace=False)} | {geo.nb - 1})  # the partial last block too
-        ref = attn_ref_rows(f64(Qb[0, h]), f64(Kb[0, h]), f64(Vb[0, h]), mask[0, h], geo, rows)
-        for i, o in ref.items():
-            errs.append(np.abs(O[h][geo.block_tokens[i]] - o).ravel())
-    e = np.concatenate(errs)
-    log(f"[curve] {name} attn: heads {heads}, max abs {e.max():.3e} mean abs {e.mean():.3e}")
-    assert e.max() <= ATTN_MAX_ABS and e.mean() <= ATTN_MEAN_ABS
+    rows = rule_rows(counts[0], geo.nb, 17)
+    emax, emean, n = attn_rule_errors(Qb, Kb, Vb, mask[0], O, geo, rows)
+    log(f"[curve] {name} attn: {describe_rows(rows)}, {n} elements compared, max abs {emax:.3e} mean abs {emean:.3e}")
+    assert emax <= ATTN_MAX_ABS and emean <= ATTN_MEAN_ABS
 
 
 def test_permute_rows_batch_two_bhnd_layout():

@@ -5,13 +5,19 @@
   read through the layout include/fva.h documents.
 * fva_attn_fp8v is compared with the fp64 oracle run on the dequantised V
   (the exact effect of the V rounding) with the same mask. The one rounding
-  the oracle does not model is that of the probabilities to E4M3 (relative
-  error u = 2^-4), which moves a normalised output by at most
-  u / (1 - u) * sum_k w_k |v_k - O'| (oracle.fp8.p_rounding_bound). Bar, per
-  element: |O - O'| <= that bound + 2e-2 (the bf16 path's own bar for the
-  Q K^T products, the softmax and the bf16 output); over all compared
-  elements: mean |O - O'| <= 1e-3 + mean of u * sqrt(sum_k w_k^2 (v_k - O')^2)
-  (the spread of the rounding sum for independent errors).
+  the oracle does not model is that of the probabilities to E4M3: relative
+  2^-4 in the format's normal range, at most half a subnormal quantum
+  (2^-17 of the row maximum) below it, the value itself where it flushes to
+  zero; oracle.fp8.p_rounding_bound turns that into a bound on each output
+  element (exact form on small cases, heavy keys exact plus a Cauchy-Schwarz
+  tail on the full-size row sets). Bar, per element: |O - O'| <= that bound +
+  1e-2, the error of the rest of the arithmetic (bf16 Q K^T products, fp32
+  softmax and accumulation, bf16 output): the bf16 path, which does the same
+  arithmetic with bf16 instead of E4M3 probabilities, stays within 8.9e-3 of
+  the fp64 oracle on every case measured (largest of its parity cases). Over
+  all compared elements: mean |O - O'| <= 1e-3 + mean of
+  sqrt(sum_k (c_k w_k)^2 (v_k - O')^2) (the spread of the rounding sum for
+  independent errors).
 """
 
 import numpy as np
@@ -21,11 +27,24 @@ import synth
 from oracle import attn_ref_rows, curve_geometry, tile_geometry
 from oracle.fp8 import dequantize_v, p_rounding_bound, quantize_v
 
-from _gpu_util import custom_config, f64, geometry_of, lib, log, tiling_of, to_dev, torch_mod, workload
+from _gpu_util import (
+    custom_config,
+    describe_rows,
+    f64,
+    geometry_of,
+    lib,
+    log,
+    map_blocks,
+    rule_rows,
+    tiling_of,
+    to_dev,
+    torch_mod,
+    workload,
+)
 
 pytestmark = pytest.mark.gpu
 
-ALLOW_BF16 = 2e-2
+ALLOW_OWN = 1e-2  # the rest of the arithmetic; the bf16 path's largest measured error is 8.9e-3
 ALLOW_MEAN = 1e-3
 
 
@@ -117,7 +136,7 @@ def compare_rows(name, Qb, Kb, Vb, mask, O, geo, rows_by_head):
     log(f"[fp8] {name}: vs dequantised-V oracle max {errs.max():.3e} mean {errs.mean():.3e} "
         f"(max excess over the P bound {over.max():.3e}, mean rms {rmss.mean():.3e}); "
         f"vs unquantised oracle max {ex.max():.3e} mean {ex.mean():.3e}")
-    assert over.max() <= ALLOW_BF16, over.max()
+    assert over.max() <= ALLOW_OWN, over.max()
     assert errs.mean() <= ALLOW_MEAN + rmss.mean(), (errs.mean(), rmss.mean())
     return errs, ex
 
@@ -181,8 +200,42 @@ def test_fp8_attn_empty_rows_and_forced_splits(s):
         compare_rows(f"empty rows, {name}", Qb, Kb, Vb, m[0], O[0], geo, kept)
 
 
+def compare_rule(name, Qb, Kb, Vb, mask, O, geo, rows):
+    """The bar of the module docstring over {head: query blocks} at full size:
+    the dequantised-V output and the bound (heavy keys exact, Cauchy-Schwarz
+    tail) from one oracle pass per block, in the thread pool."""
+    emax, esum, rsum, n, worst = 0.0, 0.0, 0.0, 0, -np.inf
+    for h, blocks in rows.items():
+        Qh, Kh = f64(Qb[0, h]), f64(Kb[0, h])
+        codes, e = quantize_v(f64(Vb[0, h]))
+        Vq = dequantize_v(codes, e)
+        mh = mask[h]
+
+        def part(chunk):
+            res = p_rounding_bound(Qh, Kh, Vq, mh, geo, chunk, method="cauchy", with_output=True)
+            out = {}
+            for i, (o_ref, bound, rms) in res.items():
+                err = np.abs(O[h][geo.block_tokens[i]] - o_ref)
+                out[i] = (float(err.max()), float(err.sum()), float(rms.sum()), int(err.size),
+                          float((err - bound).max()))
+            return out
+
+        for mx, sm, rs, cnt, ov in map_blocks(part, blocks).values():
+            emax = max(emax, mx)
+            esum += sm
+            rsum += rs
+            n += cnt
+            worst = max(worst, ov)
+    log(f"[fp8] {name}: {describe_rows(rows)}, {n} elements compared, vs dequantised-V oracle max {emax:.3e} "
+        f"mean {esum / n:.3e} (max excess over the P bound {worst:.3e}, mean rms {rsum / n:.3e})")
+    assert worst <= ALLOW_OWN, worst
+    assert esum / n <= ALLOW_MEAN + rsum / n, (esum / n, rsum / n)
+
+
 @pytest.mark.parametrize("name", ["480p", "720p", "720p_stress", "long"])
-def test_fp8_attn_full_workloads_sampled(name):
+def test_fp8_attn_full_workloads_rule(name):
+    # every query block of the lowest- and highest-density heads and of two
+    # random heads, plus 64 random (head, block) rows
     fva = lib()
     cfg = synth.get_config(name)
     Qb, Kb, Vb = workload(name)
@@ -192,11 +245,7 @@ def test_fp8_attn_full_workloads_sampled(name):
     O = fp8_attn(Qb, Kb, Vb, tiling, mask, counts, kv)
     m = mask.cpu().numpy()[0]
     c = counts.cpu().numpy()[0]
-    dens = c.mean(axis=-1)
-    rng = np.random.default_rng(29)
-    heads = [int(np.argmin(dens)), int(np.argmax(dens)), int(rng.integers(cfg.heads))]
-    rows = {h: sorted({int(i) for i in rng.choice(geo.nb, 3, replace=False)} | {geo.nb - 1}) for h in heads}
-    compare_rows(name, Qb, Kb, Vb, m, O[0], geo, rows)
+    compare_rule(name, Qb, Kb, Vb, m, O[0], geo, rule_rows(c, geo.nb, 29))
 
 
 def test_fp8_attn_deterministic():
@@ -230,11 +279,10 @@ def test_fp8_attn_hilbert_blocks(name, B):
     m = mask.cpu().numpy()[0]
     # the quantiser saw the permuted rows, whose channel maxima are the same
     assert np.array_equal(vexp.cpu().numpy()[0], np.stack([quantize_v(f64(Vb[0, h]))[1] for h in range(cfg.heads)]))
-    rng = np.random.default_rng(37)
-    heads = range(cfg.heads) if cfg.heads <= 2 else [0, int(rng.integers(cfg.heads))]
-    rows = {h: (list(range(geo.nb)) if geo.nb <= 16 else
-                sorted({int(i) for i in rng.choice(geo.nb, 3, replace=False)} | {geo.nb - 1})) for h in heads}
-    compare_rows(f"{name} hilbert", Qb, Kb, Vb, m, O[0], geo, rows)
+    if geo.nb <= 16:
+        compare_rows(f"{name} hilbert", Qb, Kb, Vb, m, O[0], geo, {h: list(range(geo.nb)) for h in range(cfg.heads)})
+    else:
+        compare_rule(f"{name} hilbert", Qb, Kb, Vb, m, O[0], geo, rule_rows(counts.cpu().numpy()[0], geo.nb, 37))
 
 
 def test_fp8_attn_batch_two_odd_heads():

@@ -5,7 +5,7 @@ floor, §3.1 pooled block similarities, Eq. 1 workload) or plain mathematics
 impose, independent of the oracle's own implementation:
 
 * pooling: explicit per-token loops, constants and linearity;
-* Top-p: brute-force subset enumeration (smallest set reaching p, and the
+* Top-p: brute-force subset enumeration (fewest blocks with mass >= p, and the
   chosen set has the largest mass among sets of that size), hand-worked rows
   (tests/golden/topp_rows.json), the uniform and one-hot closed forms;
 * invariants: floor, reach, minimality, prefix property, nesting in p.
