@@ -35,9 +35,15 @@
  *   and outputs are distinct.
  * - Supported shapes: head_dim == 128, bt*bh*bw in {64, 128}, nb <= 1024,
  *   tokens * stride_n * 2 < 2^31 (one head addressed with 32-bit byte
- *   offsets), and batch * heads <= 65535 for the routing calls,
- *   fva_quantize_v and fva_permute_tokens. Anything else returns
- *   FVA_ERR_UNSUPPORTED (there is no slow generic path).
+ *   offsets), batch * heads <= 65535 for the routing calls,
+ *   fva_quantize_v and fva_permute_tokens, and for the attention calls
+ *   batch * heads * nb plus the chunk items (2048 with the automatic chunk
+ *   size, 2^28 under FVA_SPLIT_BLOCKS, none under FVA_SCHED_NAIVE) below 2^31
+ *   (32-bit work-item indices). Anything else returns FVA_ERR_UNSUPPORTED
+ *   (there is no slow generic path).
+ * - Utility calls (fva_num_blocks, the *_workspace_size and size queries,
+ *   fva_trace_words, fva_status_string) are bookkeeping of this interface:
+ *   no passage of the paper defines them.
  */
 #ifndef FVA_H
 #define FVA_H
@@ -54,7 +60,8 @@ typedef enum fva_status {
   FVA_ERR_INVALID_ARG = -1, /* null pointer, p outside [0,1] or NaN, k_min < 0, bad flags */
   FVA_ERR_SHAPE = -2,       /* tokens != T*H*W, non-positive extents, bad strides */
   FVA_ERR_UNSUPPORTED = -3, /* head_dim != 128, tile volume not 64/128, nb > 1024, head > 2 GiB,
-                               curve grid extent > 256, batch*heads > 65535 where noted */
+                               curve grid extent > 256, batch*heads > 65535 where noted,
+                               attention work items >= 2^31 */
   FVA_ERR_WORKSPACE = -4,   /* workspace missing or smaller than the query says */
   FVA_ERR_HIP = -5          /* a kernel launch failed */
 } fva_status;
@@ -173,7 +180,8 @@ fva_status fva_attn_workspace_size(const fva_qkv_desc* desc, const fva_tiling* t
                                    size_t* bytes);
 
 /* Number of int64 words `trace` must hold under FVA_TRACE: 4 per (b, h, i)
- * row, then 4 for each of up to 2048 chunk items of split rows. */
+ * row, then 4 for each of up to 2048 chunk items of split rows; -1 for a
+ * shape the attention calls do not support. */
 int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling);
 
 /*

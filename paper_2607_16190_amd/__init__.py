@@ -20,7 +20,6 @@ attend with the one-dimensional tiling, and permute O back:
 """
 
 import ctypes
-import math
 import os
 from dataclasses import dataclass
 
@@ -431,6 +430,3 @@ def fva_attn_fp8v(q, k, v8, vexp, tiling: Tiling, mask, counts=None, kv_idx=None
     _check(st, "fva_attn_fp8v")
     return out
 
-
-def default_scale(head_dim: int = 128) -> float:
-    return 1.0 / math.sqrt(head_dim)

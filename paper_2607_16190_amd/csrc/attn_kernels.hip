@@ -25,6 +25,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "fva_common.h"
@@ -1196,12 +1197,16 @@ struct DeviceInfo {
   int per_cu8 = 0;   // same for the FP8 variant
 };
 
+// Per-device occupancy, filled on a device's first call. Calls may come from
+// several host threads at once: the cache is read and written under one lock.
 hipError_t device_info(DeviceInfo& info) {
   static DeviceInfo cache[64];
+  static std::mutex cache_lock;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> guard(cache_lock);
   if (cache[dev].cus == 0) {
     DeviceInfo d;
     e = hipDeviceGetAttribute(&d.cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -1362,7 +1367,7 @@ hipError_t launch_attn(const AttnArgs& a) {
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   int grid = info.cus * (f8 ? info.per_cu8 : info.per_cu);
-  if (grid > n_items + ws.cap) grid = n_items + ws.cap;
+  if ((int64_t)grid > (int64_t)n_items + ws.cap) grid = n_items + ws.cap;
   if (f8)
     hipLaunchKernelGGL(attn_persistent_kernel<true>, dim3(grid), dim3(kAttnThreads), 0, a.stream, P, ws.items,
                        ws.qbase, ws.qctr);

@@ -50,6 +50,15 @@ fva_status check_curve_grid(int32_t T, int32_t H, int32_t W) {
 // Scheduling bits, the trace bit and a forced chunk size in bits 8..23.
 constexpr uint32_t kAttnFlags = 3u | (0xFFFFu << 8);
 
+// Attention indexes its work items -- batch * heads * nb query blocks plus
+// the chunk items of split rows (at most 2048 with the automatic chunk size,
+// at most 2^28 under FVA_SPLIT_BLOCKS) -- and their trace records with 32-bit
+// integers.
+bool attn_items_fit(const fva_qkv_desc* d, int nb, uint32_t flags) {
+  const int64_t chunks = (flags & 1u) ? 0 : (((flags >> 8) & 0xFFFFu) ? ((int64_t)1 << 28) : 2048);
+  return (int64_t)d->batch * d->heads * nb + chunks <= (int64_t)INT32_MAX;
+}
+
 }  // namespace
 
 extern "C" {
@@ -76,13 +85,14 @@ fva_status fva_attn_workspace_size(const fva_qkv_desc* desc, const fva_tiling* t
   int nb = 0;
   const fva_status s = check_shape(desc, tiling, &nb);
   if (s != FVA_OK) return s;
+  if (!attn_items_fit(desc, nb, flags)) return FVA_ERR_UNSUPPORTED;
   *bytes = fva::attn_workspace_bytes(desc->batch, desc->heads, nb, flags);
   return FVA_OK;
 }
 
 int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling) {
   int nb = 0;
-  if (check_shape(desc, tiling, &nb) != FVA_OK) return -1;
+  if (check_shape(desc, tiling, &nb) != FVA_OK || !attn_items_fit(desc, nb, 0u)) return -1;
   return fva::attn_trace_words(desc->batch, desc->heads, nb);
 }
 
@@ -187,6 +197,7 @@ fva_status attn_common(const void* Q, const void* K, const void* V, const uint8_
   int nb = 0;
   const fva_status s = check_shape(desc, tiling, &nb);
   if (s != FVA_OK) return s;
+  if (!attn_items_fit(desc, nb, flags)) return FVA_ERR_UNSUPPORTED;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(O)) return FVA_ERR_INVALID_ARG;
   if (V && !aligned16(V)) return FVA_ERR_INVALID_ARG;
   if (V8 && !aligned16(V8)) return FVA_ERR_INVALID_ARG;

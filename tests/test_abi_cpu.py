@@ -133,6 +133,27 @@ def test_attn_argument_errors():
     assert _attn(wsb=10) == fva.FVA_ERR_WORKSPACE
 
 
+def test_attn_rejects_work_item_overflow():
+    # batch * heads * nb must leave room for the chunk items below 2^31
+    # (32-bit work-item indices): rejected on the host, before any launch.
+    big = desc(B=1024, H=3200)  # 3,276,800 heads x 660 blocks = 2.16e9 rows
+    for flags in (0, fva.FVA_SCHED_NAIVE, fva.FVA_SPLIT_BLOCKS(4)):
+        st = fva.lib.fva_attn(FAKE, FAKE, FAKE, ctypes.byref(big), ctypes.byref(T720.c()), FAKE, None, None,
+                              ctypes.c_float(0.0), flags, FAKE, FAKE, ctypes.c_size_t(1 << 62), None, None)
+        assert st == fva.FVA_ERR_UNSUPPORTED, flags
+        with pytest.raises(fva.FvaError) as e:
+            fva.fva_attn_workspace_size(big, T720, flags)
+        assert e.value.status == fva.FVA_ERR_UNSUPPORTED
+    assert fva.lib.fva_trace_words(ctypes.byref(big), ctypes.byref(T720.c())) == -1
+    # just inside the limit with the automatic chunk size, outside with forced splits
+    n_ok = (2**31 - 1 - 2048) // 660
+    ok = desc(B=1, H=n_ok)
+    assert fva.fva_attn_workspace_size(ok, T720) > 0
+    with pytest.raises(fva.FvaError):
+        fva.fva_attn_workspace_size(ok, T720, fva.FVA_SPLIT_BLOCKS(4))
+    assert fva.fva_attn_workspace_size(desc(B=1, H=n_ok + 4), T720, fva.FVA_SCHED_NAIVE) > 0
+
+
 def test_curve_workspace_sizes():
     al = lambda x: (x + 255) // 256 * 256
     # 8^k-bit bitmap and its word prefixes (max(1, 8^k / 32) words each), one index per token
