@@ -36,7 +36,13 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "sparse attn ms + dense-equiv TFLOPS, MFMA util on kept blocks; route GB/s"
-PEAK_BF16_TFLOPS = 2500.0
+PEAK_BF16_TFLOPS = 2500.0  # published dense bf16 MFMA peak
+# The same peak from the unit counts: 256 CUs x 4096 bf16 flop per clock per
+# CU; at the 2.4 GHz peak engine clock 2516.6 TFLOP/s. The line also reports
+# the fraction against this figure at the engine clock measured in the run.
+CUS = 256
+BF16_FLOP_PER_CLK_CU = 4096
+PEAK_BF16_TFLOPS_2400 = CUS * BF16_FLOP_PER_CLK_CU * 2.4e9 / 1e12
 PEAK_FP8_TFLOPS = 5000.0
 # Q K^T (bf16) and P V (fp8) are equal halves of the attention flops: at both
 # peaks a launch would take flops/2 / 2500 + flops/2 / 5000 TFLOP-seconds.
@@ -99,7 +105,10 @@ def imbalance(trace, counts):
     xc = np.bincount(tr[:rows, 2][row_used] >> 16, weights=counts.reshape(-1)[row_used].astype(np.float64),
                      minlength=8)
     span = float(tr[used, 1].max() - tr[used, 0].min()) / 100.0  # 100 MHz clock -> us
+    # engine clock: shader cycles (word 3) over the 100 MHz constant clock
+    sclk = float(tr[used, 3].sum()) * 100.0 / float((tr[used, 1] - tr[used, 0]).sum())
     return {
+        "sclk_mhz": round(sclk, 1),
         "cus_used": int(busy.size),
         "cu_busy_max_over_mean": round(float(busy.max() / busy.mean()), 4),
         "xcd_time_rho": round(float(xb.max() / xb.mean()), 4),
@@ -189,6 +198,103 @@ ROUTE_TRAFFIC = {
 }
 
 
+def extra_workloads(torch, fva, synth, dev, reps=3):
+    """The other two timed workloads, outside the timed region, as extra keys.
+
+    long: the 31x45x80 clip (111,600 tokens, nb 960) at p = 0.8, 0.9 and 0.95:
+    retained fraction, route and attention times (HIP events, mean of reps
+    after one warmup each).
+    720p_stress: 8 flat and 32 concentrated heads of the 720p shape: attention
+    time under the persistent scheduler and under the naive head-major grid,
+    and from one traced run of each the per-CU busy max/mean, the per-XCD
+    imbalance and the span (Eq. 2 with XCDs as ranks).
+    """
+    stream = torch.cuda.current_stream()
+    out = {}
+
+    def load(name):
+        cfg = synth.get_config(name)
+        log(f"[bench] extra workload {name}: generating {cfg.heads} heads x {cfg.N} tokens")
+        Qb, Kb, Vb = synth.gen_qkv(cfg)
+        up = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        q, k, v = up(Qb), up(Kb), up(Vb)
+        del Qb, Kb, Vb
+        tiling = fva.Tiling(*cfg.grid, *cfg.tile)
+        nb = fva.fva_num_blocks(tiling)
+        B, H = q.shape[0], q.shape[1]
+        bufs = dict(mask=torch.empty((B, H, nb, nb), dtype=torch.uint8, device=dev),
+                    counts=torch.empty((B, H, nb), dtype=torch.int32, device=dev),
+                    kv=torch.empty((B, H, nb, nb), dtype=torch.int32, device=dev),
+                    out=torch.empty_like(q),
+                    ws_r=torch.empty(fva.fva_route_workspace_size(fva._desc_of(q), tiling), dtype=torch.uint8,
+                                     device=dev),
+                    ws_a=torch.empty(fva.fva_attn_workspace_size(fva._desc_of(q), tiling), dtype=torch.uint8,
+                                     device=dev))
+        return cfg, tiling, nb, (q, k, v), bufs
+
+    def timed_pair(route_fn, attn_fn):
+        route_fn()
+        attn_fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        tr, ta = 0.0, 0.0
+        for _ in range(reps):
+            ev[0].record(stream)
+            route_fn()
+            ev[1].record(stream)
+            attn_fn()
+            ev[2].record(stream)
+            torch.cuda.synchronize()
+            tr += ev[0].elapsed_time(ev[1])
+            ta += ev[1].elapsed_time(ev[2])
+        return tr / reps, ta / reps
+
+    # long clip: retained fraction vs time over the p sweep
+    cfg, tiling, nb, (q, k, v), b = load("long")
+    sweep = []
+    for pp in (0.8, 0.9, 0.95):
+        route_fn = lambda: fva.fva_route(q, k, pp, cfg.k_min, tiling, out=(b["mask"], b["counts"], b["kv"]),
+                                         workspace=b["ws_r"])
+        attn_fn = lambda: fva.fva_attn(q, k, v, tiling, b["mask"], b["counts"], b["kv"], out=b["out"],
+                                       workspace=b["ws_a"])
+        t_r, t_a = timed_pair(route_fn, attn_fn)
+        kept = int(b["counts"].sum().item())
+        dense = 4.0 * q.shape[1] * float(cfg.N) ** 2 * 128
+        sweep.append({"p": pp, "retained_fraction": round(kept / (q.shape[1] * nb * nb), 4),
+                      "route_us": round(t_r * 1e3, 1), "attn_ms": round(t_a, 3),
+                      "kept_tile_TFLOPS": round(4.0 * 128**3 * kept / (t_a / 1e3) / 1e12, 1),
+                      "dense_equiv_TFLOPS": round(dense / ((t_r + t_a) / 1e3) / 1e12, 1)})
+        log(f"[bench] long p={pp}: {sweep[-1]}")
+    out["long_p_sweep"] = {"workload": f"long: {q.shape[1]} heads, 31x45x80 = {cfg.N} tokens, tile 2x8x8, nb={nb}, "
+                                       f"k_min={cfg.k_min}", "reps": reps, "points": sweep}
+    del q, k, v, b
+    torch.cuda.empty_cache()
+
+    # stress: persistent scheduler against the naive head-major grid
+    cfg, tiling, nb, (q, k, v), b = load("720p_stress")
+    fva.fva_route(q, k, cfg.p, cfg.k_min, tiling, out=(b["mask"], b["counts"], b["kv"]), workspace=b["ws_r"])
+    c_np = b["counts"].cpu().numpy()
+    res = {"workload": f"720p_stress: {q.shape[1]} heads (8 at alpha 0.3, 32 at alpha 5), 21x45x80, tile 2x8x8, "
+                       f"nb={nb}, p={cfg.p}, k_min={cfg.k_min}",
+           "retained_fraction": round(float(c_np.sum()) / (q.shape[1] * nb * nb), 4)}
+    tw = fva.fva_trace_words(fva._desc_of(q), tiling)
+    trace = torch.zeros(tw, dtype=torch.int64, device=dev)
+    for name, fl in (("persistent", fva.FVA_SCHED_PERSISTENT), ("naive", fva.FVA_SCHED_NAIVE)):
+        attn_fn = lambda: fva.fva_attn(q, k, v, tiling, b["mask"], b["counts"], b["kv"], flags=fl, out=b["out"],
+                                       workspace=b["ws_a"])
+        _, t_a = timed_pair(lambda: None, attn_fn)
+        trace.zero_()
+        fva.fva_attn(q, k, v, tiling, b["mask"], b["counts"], b["kv"], flags=fl | fva.FVA_TRACE, out=b["out"],
+                     workspace=b["ws_a"], trace=trace)
+        torch.cuda.synchronize()
+        res[name] = {"attn_ms": round(t_a, 3), **imbalance(trace.cpu().numpy(), c_np)}
+        log(f"[bench] stress {name}: {res[name]}")
+    out["stress_scheduler"] = res
+    del q, k, v, b, trace
+    torch.cuda.empty_cache()
+    return out
+
+
 def copy_calibration(torch, gib=1.0, reps=5):
     """Plain device copy of known size (reads and writes `gib` GiB each)."""
     n = int(gib * (1 << 30))
@@ -266,6 +372,8 @@ def main():
     ap.add_argument("--flushed-reps", type=int, default=20,
                     help="steps timed one by one after a 512 MB cache-flushing write, outside the timed region (0: skip)")
     ap.add_argument("--copy-calibration", action="store_true", help="only time a 1 GiB device copy")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the long-clip p sweep and the stress scheduler comparison (extra keys)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -515,6 +623,8 @@ def main():
         },
         "kept_tile_TFLOPS": round(kept_tile_flops / t_attn / 1e12, 2),
         "kept_tile_frac_bf16_peak": round(kept_tile_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "kept_tile_frac_bf16_2516": round(kept_tile_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS_2400, 4),
+        "useful_frac_bf16_2516": round(useful_flops / t_attn / 1e12 / PEAK_BF16_TFLOPS_2400, 4),
         "kept_tile_frac_peak": round(kept_tile_flops / t_attn / 1e12 / peak, 4),
         "useful_TFLOPS": round(useful_flops / t_attn / 1e12, 2),
         "dense_equiv_attn_TFLOPS": round(dense_flops / t_attn / 1e12, 2),
@@ -608,6 +718,17 @@ def main():
             imb[name] = imbalance(trace.cpu().numpy(), c_np)
         res["scheduler_trace"] = imb
         log(f"[bench] trace: {imb}")
+        # engine clock of the traced persistent run, and the attention's
+        # fraction of the peak at that clock
+        sclk = imb["persistent"]["sclk_mhz"]
+        res["sclk_mhz"] = sclk
+        peak_clk = CUS * BF16_FLOP_PER_CLK_CU * sclk * 1e6 / 1e12
+        if not fp8:
+            res["roofline"]["peak_at_sclk"] = round(peak_clk, 1)
+            res["roofline"]["frac_at_sclk"] = round(useful_flops / t_attn / 1e12 / peak_clk, 4)
+            res["kept_tile_frac_at_sclk"] = round(kept_tile_flops / t_attn / 1e12 / peak_clk, 4)
+    if not args.no_extra and args.workload == "720p" and not args.sasa:
+        res.update(extra_workloads(torch, fva, synth, dev))
     if args.p_sweep:
         sweep = []
         for pp in [float(x) for x in args.p_sweep.split(",")]:

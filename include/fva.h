@@ -205,10 +205,12 @@ int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling);
  *        so results stay deterministic.
  * O: bf16, same strides as Q; every real token row is written.
  * trace: device int64 [fva_trace_words] when FVA_TRACE is set, else ignored.
- *        Row r = (b*heads + h)*nb + i gets {start clock, end clock,
- *        (xcc_id << 16) | hw_id low bits, workgroup id} (unwritten for a
- *        split row), chunk c of a split row the same at batch*heads*nb + c
- *        (c < 2048); clocks are the 100 MHz constant device clock.
+ *        Row r = (b*heads + h)*nb + i gets {start, end, (xcc_id << 16) |
+ *        hw_id low bits, shader-clock cycles} (unwritten for a split row),
+ *        chunk c of a split row the same at batch*heads*nb + c (c < 2048);
+ *        start and end are the 100 MHz constant device clock, the last word
+ *        the item's elapsed engine-clock cycles (s_memtime), so that
+ *        cycles * 100 MHz / (end - start) is the engine clock it ran at.
  */
 fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_desc* desc,
                     const fva_tiling* tiling, const uint8_t* block_mask, const int32_t* counts,

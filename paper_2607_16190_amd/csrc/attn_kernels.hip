@@ -804,15 +804,19 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   }
 }
 
-// Trace record r: rows first, then chunk items (chunk c at n_rows + c).
-__device__ __forceinline__ void trace_item(const AttnParams& P, int64_t rec, int64_t t0) {
+// Trace record r: rows first, then chunk items (chunk c at n_rows + c):
+// start and end on the 100 MHz constant clock, where the item ran, and the
+// shader-clock cycles (s_memtime) it took, so that the engine clock of the
+// run is the ratio of the two clocks.
+__device__ __forceinline__ void trace_item(const AttnParams& P, int64_t rec, int64_t t0, int64_t c0) {
   if (P.trace && threadIdx.x == 0) {
+    const int64_t c1 = (int64_t)__builtin_amdgcn_s_memtime();
     const int64_t t1 = (int64_t)wall_clock64();
     int64_t* tr = P.trace + rec * 4;
     tr[0] = t0;
     tr[1] = t1;
     tr[2] = (int64_t)hw_location();
-    tr[3] = (int64_t)blockIdx.x;
+    tr[3] = c1 - c0;
   }
 }
 
@@ -821,10 +825,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams 
   __shared__ __align__(16) unsigned char ks_tile[kTileBytes];
   __shared__ __align__(16) unsigned char vs_tile[F8 ? kV8TileBytes : kTileBytes];
   const int64_t t0 = (int64_t)wall_clock64();
+  const int64_t c0 = P.trace ? (int64_t)__builtin_amdgcn_s_memtime() : 0;
   process_item<F8>(P, blockIdx.x, 0, P.g.nb, nullptr, ks_tile, vs_tile);
   if (P.trace) {
     __syncthreads();
-    trace_item(P, blockIdx.x, t0);
+    trace_item(P, blockIdx.x, t0, c0);
   }
 }
 
@@ -870,6 +875,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
     // item >= 0: a whole row; item < 0: chunk -1 - item of a split row
     const int item = __builtin_amdgcn_readfirstlane(items[slot]);
     const int64_t t0 = (int64_t)wall_clock64();
+    const int64_t c0 = P.trace ? (int64_t)__builtin_amdgcn_s_memtime() : 0;
     int64_t rec;
     if (item >= 0) {
       process_item<F8>(P, item, 0, P.g.nb, nullptr, ks_tile, vs_tile);
@@ -882,7 +888,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
       rec = c < P.trace_chunks ? P.n_rows + c : -1;
     }
     __syncthreads();  // the next item's copies overwrite the tiles; next_slot is rewritten
-    if (P.trace && rec >= 0) trace_item(P, rec, t0);
+    if (P.trace && rec >= 0) trace_item(P, rec, t0, c0);
   }
 }
 

@@ -200,6 +200,10 @@ def test_attn_deterministic_and_trace():
     assert tr.shape[0] == rows + 2048  # rows, then chunk records (no row is split here)
     assert np.all(tr[:rows, 1] >= tr[:rows, 0]) and np.all(tr[:rows, 0] > 0)
     assert not tr[rows:].any()
+    # engine clock of the run: shader cycles over the 100 MHz clock
+    sclk = tr[:rows, 3].sum() * 100.0 / (tr[:rows, 1] - tr[:rows, 0]).sum()
+    log(f"[attn] 720p trace: engine clock {sclk:.0f} MHz")
+    assert np.all(tr[:rows, 3] > 0) and 500.0 < sclk < 3000.0
 
 
 def test_attn_max_blocks_sampled():
