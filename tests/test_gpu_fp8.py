@@ -313,4 +313,4 @@ def test_fp8_attn_max_blocks_sampled():
     mask, counts, kv = fva.fva_route(to_dev(Qb), to_dev(Kb), cfg.p, cfg.k_min, t)
     O = fp8_attn(Qb, Kb, Vb, t, mask, counts, kv)
     rows = {0: [0, 511, 777, 1023]}
-    compare_rows("max blocks", Qb, Kb, Vb, mask.cpu().numpy()[0], O[0], geo, rows)
+    compare_rule("max blocks", Qb, Kb, Vb, mask.cpu().numpy()[0], O[0], geo, rows)
