@@ -63,7 +63,8 @@ typedef enum fva_status {
                                curve grid extent > 256, batch*heads > 65535 where noted,
                                attention work items >= 2^31 */
   FVA_ERR_WORKSPACE = -4,   /* workspace missing or smaller than the query says */
-  FVA_ERR_HIP = -5          /* a kernel launch failed */
+  FVA_ERR_HIP = -5,         /* a kernel launch failed */
+  FVA_ERR_SCRATCH = -6      /* fva_attn_noalloc: the shape needs more than the static scratch */
 } fva_status;
 
 /* Latent grid (T x H x W) and 3D block box (bt x bh x bw). */
@@ -328,6 +329,36 @@ fva_status fva_attn_fp8v(const void* Q, const void* K, const uint8_t* V8, const 
                          const fva_qkv_desc* desc, const fva_tiling* tiling, const uint8_t* block_mask,
                          const int32_t* counts, const int32_t* kv_idx, float softmax_scale, uint32_t flags, void* O,
                          void* workspace, size_t workspace_bytes, void* trace, void* stream);
+
+/*
+ * Allocation-free attention, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): fva_attn with the persistent scheduler, whose work list, plan
+ * scratch and block records live in a static device array of the library
+ * (16 MiB on every device the library runs on, held until the process
+ * ends) instead of a caller workspace. The call allocates nothing.
+ *
+ * Differences from fva_attn: counts and kv_idx are required (in the layout
+ * fva_route writes; the mask itself is not read); flags may hold FVA_TRACE
+ * only (FVA_SCHED_NAIVE and FVA_SPLIT_BLOCKS are rejected); no row is split
+ * into chunks, so where fva_attn's automatic chunk size would split rows
+ * (few rows per workgroup slot) the output can differ from fva_attn's in the
+ * last bits (the same sums in another order); everywhere else it is
+ * identical. Inputs, O, trace and errors as for fva_attn.
+ *
+ * A shape needs, of the 16 MiB, the queue items (4 bytes per query block),
+ * two per-row prefixes (8 bytes per query block + 8), 76 bytes per head,
+ * 32 bytes per block of the tiling and 80 bytes of queue bookkeeping, each
+ * part rounded up to 256 bytes: with nb = 660 about 2,000 heads fit. A
+ * shape needing more returns FVA_ERR_SCRATCH before anything is launched.
+ * Every call on one device shares that
+ * device's scratch, and the plan kernel rewrites all of it on every call:
+ * calls that overlap on one device (different streams, or host threads)
+ * race and give undefined results; calls in one stream order are safe.
+ */
+fva_status fva_attn_noalloc(const void* Q, const void* K, const void* V, const fva_qkv_desc* desc,
+                            const fva_tiling* tiling, const int32_t* counts, const int32_t* kv_idx,
+                            float softmax_scale, uint32_t flags, void* O, void* trace, void* stream);
 
 /* Static description of a status code. */
 const char* fva_status_string(fva_status status);

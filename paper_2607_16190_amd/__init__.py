@@ -32,6 +32,7 @@ FVA_ERR_SHAPE = -2
 FVA_ERR_UNSUPPORTED = -3
 FVA_ERR_WORKSPACE = -4
 FVA_ERR_HIP = -5
+FVA_ERR_SCRATCH = -6
 
 FVA_SCHED_PERSISTENT = 0
 FVA_SCHED_NAIVE = 1
@@ -61,6 +62,7 @@ EXPORTED = (
     "fva_quantize_v_workspace_size",
     "fva_quantize_v",
     "fva_attn_fp8v",
+    "fva_attn_noalloc",
     "fva_status_string",
 )
 
@@ -155,6 +157,10 @@ def _load():
         "fva_attn_fp8v": (
             ctypes.c_int,
             [P, P, P, P, D, T, P, P, P, ctypes.c_float, ctypes.c_uint32, P, P, ctypes.c_size_t, P, P],
+        ),
+        "fva_attn_noalloc": (
+            ctypes.c_int,
+            [P, P, P, D, T, P, P, ctypes.c_float, ctypes.c_uint32, P, P, P],
         ),
         "fva_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     }
@@ -320,6 +326,32 @@ def fva_attn(q, k, v, tiling: Tiling, mask, counts=None, kv_idx=None, *, scale: 
         ctypes.c_size_t(ws.numel() * ws.element_size()), _ptr(trace), _stream_ptr(torch, stream),
     )
     _check(st, "fva_attn")
+    return out
+
+
+def fva_attn_noalloc(q, k, v, tiling: Tiling, counts, kv_idx, out, *, scale: float = 0.0, flags: int = 0,
+                     trace=None, stream=None):
+    """fva_attn on the library's static scratch (see include/fva.h): no device
+    allocation in the library or here; the caller passes every buffer,
+    including `out`."""
+    import torch
+
+    for t in (q, k, v, out):
+        if t.dtype != torch.bfloat16 or not t.is_cuda:
+            raise ValueError("q, k, v, out must be bf16 device tensors")
+    if not (q.shape == k.shape == v.shape == out.shape) or not (q.stride() == k.stride() == v.stride() == out.stride()):
+        raise ValueError("q, k, v, out must share shape and strides")
+    for t in (counts, kv_idx):
+        if t is None or t.dtype != torch.int32 or not t.is_cuda:
+            raise ValueError("counts and kv_idx must be int32 device tensors")
+    if (flags & FVA_TRACE) and trace is None:
+        raise ValueError("FVA_TRACE needs a trace tensor of fva_trace_words int64")
+    desc = _desc_of(q)
+    st = lib.fva_attn_noalloc(
+        _ptr(q), _ptr(k), _ptr(v), ctypes.byref(desc), ctypes.byref(tiling.c()), _ptr(counts), _ptr(kv_idx),
+        ctypes.c_float(scale), int(flags), _ptr(out), _ptr(trace), _stream_ptr(torch, stream),
+    )
+    _check(st, "fva_attn_noalloc")
     return out
 
 

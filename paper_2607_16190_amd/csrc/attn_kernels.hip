@@ -1264,19 +1264,22 @@ int chunk_cap(int batch, int heads, int nb, uint32_t flags) {
   return (int)std::min<int64_t>(cap, (int64_t)1 << 28);
 }
 
-AttnWorkspace carve(void* base, int batch, int heads, int nb, uint32_t flags) {
+// lean: the layout of the allocation-free call -- no room for rebuilt counts
+// and kept lists (the caller passes them) and no chunk items (no row is
+// split, so no partial results are kept).
+AttnWorkspace carve(void* base, int batch, int heads, int nb, uint32_t flags, bool lean = false) {
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t rows = (size_t)batch * heads * nb;
   const size_t nh = (size_t)batch * heads;
   char* p = reinterpret_cast<char*>(base);
   AttnWorkspace w;
-  w.cap = chunk_cap(batch, heads, nb, flags);
+  w.cap = lean ? 0 : chunk_cap(batch, heads, nb, flags);
   const size_t cap = (size_t)w.cap;
   size_t off = 0;
-  w.counts = reinterpret_cast<int32_t*>(p + off);
-  off += al(rows * 4);
-  w.kv = reinterpret_cast<int32_t*>(p + off);
-  off += al(rows * nb * 4);
+  w.counts = lean ? nullptr : reinterpret_cast<int32_t*>(p + off);
+  off += lean ? 0 : al(rows * 4);
+  w.kv = lean ? nullptr : reinterpret_cast<int32_t*>(p + off);
+  off += lean ? 0 : al(rows * nb * 4);
   w.items = reinterpret_cast<int32_t*>(p + off);
   off += al((rows + cap) * 4);
   w.qbase = reinterpret_cast<int32_t*>(p + off);
@@ -1306,6 +1309,42 @@ size_t attn_workspace_bytes(int batch, int heads, int nb, uint32_t flags) {
   return carve(nullptr, batch, heads, nb, flags).bytes;
 }
 
+// ---- Allocation-free attention ---------------------------------------------
+// The plan, queue and block-table scratch of fva_attn_noalloc lives in this
+// file-scope device array (each device holds its own copy for the life of
+// the process). Its device address is taken once per device with that device
+// current and kept; host code passes only that address to kernels, never
+// the array's name, which is a host-side stand-in.
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+size_t attn_noalloc_bytes(int batch, int heads, int nb) {
+  return carve(nullptr, batch, heads, nb, 0u, true).bytes;
+}
+
+size_t attn_noalloc_capacity() { return kNoAllocScratchBytes; }
+
+namespace {
+hipError_t scratch_address(void** out) {
+  static void* addr[64] = {};
+  static std::mutex lock;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> guard(lock);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
+}  // namespace
+
 int64_t attn_trace_words(int batch, int heads, int nb) {
   return 4 * ((int64_t)batch * heads * nb + 4 * kSplitSlots);
 }
@@ -1315,7 +1354,7 @@ hipError_t launch_attn(const AttnArgs& a) {
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
   const int n_items = a.batch * a.heads * g.nb;
   if (n_items == 0) return hipSuccess;
-  const AttnWorkspace ws = carve(a.workspace, a.batch, a.heads, g.nb, a.flags);
+  const AttnWorkspace ws = carve(a.workspace, a.batch, a.heads, g.nb, a.flags, a.lean);
   int32_t* ws_counts = ws.counts;
   int32_t* ws_kv = ws.kv;
   DeviceInfo info;
@@ -1389,6 +1428,14 @@ hipError_t launch_attn(const AttnArgs& a) {
     e = hipGetLastError();
   }
   return e;
+}
+
+hipError_t launch_attn_noalloc(const AttnArgs& a) {
+  AttnArgs b = a;
+  hipError_t e = scratch_address(&b.workspace);
+  if (e != hipSuccess) return e;
+  b.lean = true;
+  return launch_attn(b);
 }
 
 }  // namespace fva

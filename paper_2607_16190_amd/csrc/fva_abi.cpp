@@ -245,6 +245,49 @@ fva_status fva_attn(const void* Q, const void* K, const void* V, const fva_qkv_d
                      workspace, workspace_bytes, trace, stream);
 }
 
+fva_status fva_attn_noalloc(const void* Q, const void* K, const void* V, const fva_qkv_desc* desc,
+                            const fva_tiling* tiling, const int32_t* counts, const int32_t* kv_idx,
+                            float softmax_scale, uint32_t flags, void* O, void* trace, void* stream) {
+  if (!Q || !K || !V || !O || !counts || !kv_idx) return FVA_ERR_INVALID_ARG;
+  if (flags & ~FVA_TRACE) return FVA_ERR_INVALID_ARG;  // persistent scheduler, automatic chunks only
+  if ((flags & FVA_TRACE) && !trace) return FVA_ERR_INVALID_ARG;
+  if (std::isnan(softmax_scale) || std::isinf(softmax_scale)) return FVA_ERR_INVALID_ARG;
+  int nb = 0;
+  const fva_status s = check_shape(desc, tiling, &nb);
+  if (s != FVA_OK) return s;
+  if (!attn_items_fit(desc, nb, 1u)) return FVA_ERR_UNSUPPORTED;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return FVA_ERR_INVALID_ARG;
+  if (fva::attn_noalloc_bytes(desc->batch, desc->heads, nb) > fva::attn_noalloc_capacity()) return FVA_ERR_SCRATCH;
+  fva::AttnArgs a;
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.V8 = nullptr;
+  a.vexp = nullptr;
+  a.O = O;
+  a.batch = desc->batch;
+  a.heads = desc->heads;
+  a.tokens = desc->tokens;
+  a.stride_b = desc->stride_b;
+  a.stride_h = desc->stride_h;
+  a.stride_n = desc->stride_n;
+  a.T = tiling->T;
+  a.H = tiling->H;
+  a.W = tiling->W;
+  a.bt = tiling->bt;
+  a.bh = tiling->bh;
+  a.bw = tiling->bw;
+  a.mask = nullptr;
+  a.counts = counts;
+  a.kv_idx = kv_idx;
+  a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt(128.0f);
+  a.flags = flags;
+  a.trace = reinterpret_cast<int64_t*>(trace);
+  a.workspace = nullptr;  // the library's static scratch
+  a.stream = reinterpret_cast<hipStream_t>(stream);
+  return fva::launch_attn_noalloc(a) == hipSuccess ? FVA_OK : FVA_ERR_HIP;
+}
+
 fva_status fva_v8_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes) {
   if (!bytes) return FVA_ERR_INVALID_ARG;
   int nb = 0;
@@ -349,6 +392,7 @@ const char* fva_status_string(fva_status status) {
     case FVA_ERR_UNSUPPORTED: return "unsupported shape (head_dim must be 128, tile volume 64 or 128, nb <= 1024, curve grid extents <= 256)";
     case FVA_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case FVA_ERR_HIP: return "HIP launch failed";
+    case FVA_ERR_SCRATCH: return "shape needs more scratch than the library's static device scratch holds (fva_attn_noalloc)";
   }
   return "unknown status";
 }

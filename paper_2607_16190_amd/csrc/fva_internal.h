@@ -46,6 +46,7 @@ struct AttnArgs {
   int64_t* trace;  // null unless tracing
   void* workspace;
   hipStream_t stream;
+  bool lean = false;  // workspace laid out without list copies and chunk items
 };
 
 struct QuantizeArgs {
@@ -66,6 +67,13 @@ int64_t attn_trace_words(int batch, int heads, int nb);
 
 hipError_t launch_route(const RouteArgs& a);
 hipError_t launch_attn(const AttnArgs& a);
+
+// Allocation-free attention: scratch bytes a shape needs, the capacity of
+// the library's static device scratch, and the launch (persistent scheduler,
+// caller's counts and kept lists, no split rows) on that scratch.
+size_t attn_noalloc_bytes(int batch, int heads, int nb);
+size_t attn_noalloc_capacity();
+hipError_t launch_attn_noalloc(const AttnArgs& a);
 
 // E4M3 V quantisation for the FP8 attention variant (fp8_kernels.hip).
 size_t quantize_v_workspace_bytes(int batch, int heads);

@@ -270,3 +270,41 @@ def test_host_tensors_are_refused_no_cpu_fallback():
         fva.fva_quantize_v(q, t)
     with pytest.raises(ValueError):
         fva.fva_route_sasa(q, q, 0.9, 2, t, torch.zeros(2, dtype=torch.int32), 2, 0.8, 0.07)
+
+
+def _noalloc(d=None, flags=0, counts=FAKE, kv=FAKE, trace=None, scale=0.0, o=FAKE, v=FAKE):
+    d = d or desc()
+    return fva.lib.fva_attn_noalloc(FAKE, FAKE, v, ctypes.byref(d), ctypes.byref(T720.c()), counts, kv,
+                                    ctypes.c_float(scale), flags, o, trace, None)
+
+
+def noalloc_scratch_bytes(heads, nb, batch=1):
+    """The layout include/fva.h documents for fva_attn_noalloc's scratch."""
+    al = lambda x: (x + 255) // 256 * 256
+    rows = batch * heads * nb
+    # queue items, 9 queue bases, 8 counters, per-head plan scratch, per-row
+    # prefixes, split count, one 32-byte record per block
+    return (al(rows * 4) + al(36) + al(32) + al(batch * heads * 19 * 4) + al(2 * (rows + 1) * 4) + al(4)
+            + al(nb * 32))
+
+
+def test_noalloc_scratch_limit_and_argument_errors():
+    cap = 16 << 20
+    nb = 660
+    h_ok = max(h for h in range(1, 4000) if noalloc_scratch_bytes(h, nb) <= cap)
+    assert 2000 < h_ok < 2200  # "about 2,000 heads fit" at nb = 660
+    # one head past the limit: rejected before any launch (the fake pointers
+    # are never touched); shapes inside it would launch, so none is called here
+    assert _noalloc(d=desc(H=h_ok + 1)) == fva.FVA_ERR_SCRATCH
+    assert _noalloc(d=desc(B=2, H=h_ok)) == fva.FVA_ERR_SCRATCH
+    assert "static" in fva.fva_status_string(fva.FVA_ERR_SCRATCH)
+    assert _noalloc(flags=fva.FVA_SCHED_NAIVE) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(flags=fva.FVA_SPLIT_BLOCKS(4)) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(flags=fva.FVA_TRACE, trace=None) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(counts=None) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(kv=None) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(v=None) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(o=None) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(scale=float("inf")) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(d=desc(N=10)) == fva.FVA_ERR_SHAPE
+    assert _noalloc(d=desc(B=1024, H=3200)) == fva.FVA_ERR_UNSUPPORTED
