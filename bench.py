@@ -177,12 +177,9 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "bea204804a891f72",
+    "source_digest": "328ec870179bac85",
     "bytes": {
-        "720p": (116721688 * 2 + 757109) * 1024,
-        "720p-hilbert": (79169325 * 2 + 757235) * 1024,
-        "720p-fp8v": (71441940 * 2 + 758050) * 1024,
-        "720p-hilbert-fp8v": (68150692 * 2 + 758019) * 1024,
+        "720p": ((116469693 + 116661405) // 2 * 2 + 757114) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
