@@ -413,21 +413,27 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   // the online softmax, and the PV product. A short half (the second half of
   // a block with 65 .. 96 keys) has only its first group of 32 keys: the
   // steps of the second group are skipped by uniform branches, so there is
-  // one code path for both shapes. The K (V) fragment of step u + 3 is read
-  // while step u multiplies (a ring of four fragments), so the LDS latency is
-  // covered by six MFMAs.
+  // one code path for both shapes. The K (V) fragment of step u + 2 is read
+  // while step u multiplies (a ring of three fragments), so the LDS latency
+  // is covered by four MFMAs.
   auto s_phase = [&](int hb, bool short_half, f32x4 (&s)[4][2]) {
-    constexpr int kKPre = 3;
+    constexpr int kKPre = 2;
     bf16x8 kq[kKPre + 1];
 #pragma unroll
-    for (int u = 0; u < kKPre; ++u) kq[u] = kfrag(4 * hb + (u >> 2), u & 3);
+    for (int u = 0; u < kKPre; ++u) kq[u] = kfrag(4 * hb + 2 * (u >> 3) + (u & 1), (u & 7) >> 1);
     // Issue priority while multiplying: the SIMD's other wave (another
     // workgroup, usually in its softmax) fills the matrix unit's gaps.
     __builtin_amdgcn_s_setprio(2);
+    // Step u of a group of eight (u / 8 = pair of 16-key tiles) takes tile
+    // 2 (u / 8) + u % 2 at head-dim step (u % 8) / 2: four independent
+    // accumulation chains (two tiles x two query tiles) alternate, so a
+    // dependent product never follows its predecessor directly.
+    auto t_of = [](int u) { return 2 * (u >> 3) + (u & 1); };
+    auto ks_of = [](int u) { return (u & 7) >> 1; };
     auto step = [&](auto u_c) {
       constexpr int u = decltype(u_c)::value;
-      constexpr int t = u >> 2, ks = u & 3;
-      if (u + kKPre < 16) kq[(u + kKPre) % (kKPre + 1)] = kfrag(4 * hb + ((u + kKPre) >> 2), (u + kKPre) & 3);
+      constexpr int t = 2 * (u >> 3) + (u & 1), ks = (u & 7) >> 1;
+      if (u + kKPre < 16) kq[(u + kKPre) % (kKPre + 1)] = kfrag(4 * hb + t_of(u + kKPre), ks_of(u + kKPre));
       const bf16x8 ka = kq[u % (kKPre + 1)];
       const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
       s[t][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[0][ks], ks == 0 ? z : s[t][0], 0, 0, 0);
@@ -511,7 +517,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   // also take the exponentials of the second 32 keys, two values a step, so
   // that VALU work runs while the matrix unit multiplies.
   auto pv_phase = [&](int hb, bool short_half, bf16x8 (&pb)[2][2], f32x4 (&s)[4][2], const float (&negm)[2]) {
-    constexpr int kVPre = 3;
+    constexpr int kVPre = 2;
     bf16x8 vq[kVPre + 1];
 #pragma unroll
     for (int u = 0; u < kVPre; ++u) vq[u] = vfrag(2 * hb + (u >> 3), u & 7);
