@@ -148,8 +148,10 @@ fva_status fva_route(const void* Q, const void* K, const fva_qkv_desc* desc, dou
  * the result is deterministic; the rank loads S_r + H_r * nb * e_r never
  * exceed S_max (no new straggler, n1 <= 1).
  */
-/* Workspace of fva_route_sasa: that of fva_route plus batch*heads int32,
- * 256-byte aligned. Host only. */
+/* Workspace of fva_route_sasa: that of fva_route, plus batch*heads int32
+ * (extra blocks per head) and a 16-byte record per routed row (the row's
+ * last kept block after the first pass, from which the augmentation ranks
+ * the blocks after it), each part 256-byte aligned. Host only. */
 fva_status fva_route_sasa_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, size_t* bytes);
 
 /*

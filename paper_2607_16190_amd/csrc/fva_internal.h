@@ -24,6 +24,7 @@ struct RouteArgs {
   double n1 = 0.0, n2 = 0.0;
   int32_t* rank_extra = nullptr;  // [n_ranks] extra blocks per row of each rank (device) or null
   int32_t* extra_head = nullptr;  // [batch * heads] workspace tail
+  void* row_cuts = nullptr;       // [batch * heads * nb] last kept block of each routed row (augmentation)
   void* workspace;
   hipStream_t stream;
 };

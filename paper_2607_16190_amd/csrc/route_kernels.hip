@@ -353,10 +353,23 @@ __device__ Cut select_cut(const double (&s)[KPL], const uint64_t (&F)[KPL], uint
 }
 
 template <int KPL>
+__device__ __forceinline__ void emit_row(const double (&s)[KPL], int nb, int m, const Cut& cut,
+                                         uint8_t* __restrict__ mrow, int32_t* __restrict__ count_out,
+                                         int32_t* __restrict__ kvrow, WaveScratch& ws, int lane);
+
+// Cut of a routed row, kept for the slack-aware augmentation: the score and
+// id of its last kept block.
+struct RowCut {
+  double s;
+  int j;
+  int pad;
+};
+
+template <int KPL>
 __device__ __forceinline__ void select_row(const double* __restrict__ srow, int nb, double p, int k_min,
                                            uint8_t* __restrict__ mrow, int32_t* __restrict__ count_out,
                                            int32_t* __restrict__ kvrow, WaveScratch& ws, int lane,
-                                           int m_force = -1) {
+                                           int m_force = -1, RowCut* cut_out = nullptr) {
   double s[KPL];
   uint64_t F[KPL];
   uint32_t valid = 0;
@@ -419,9 +432,21 @@ __device__ __forceinline__ void select_row(const double* __restrict__ srow, int 
   const int m = m_force >= 0 ? m_p : (m_p > kf ? m_p : kf);
   if (m > 0 && m < nb && (m != m_p || m_force >= 0))
     cut = select_cut<KPL>(s, F, valid, nb, smin, smax, zs, false, (uint64_t)m, ws, lane);
+  if (cut_out && lane == 0) {
+    // the row's last kept block in (score desc, id asc) order; none kept:
+    // +inf, so that every block ranks after it
+    cut_out->s = m <= 0 ? (double)INFINITY : m >= nb ? -(double)INFINITY : cut.s;
+    cut_out->j = m <= 0 ? -1 : m >= nb ? nb : cut.j;
+  }
+  emit_row<KPL>(s, nb, m, cut, mrow, count_out, kvrow, ws, lane);
+}
 
-  // Kept blocks: the first m of (score desc, id asc), i.e. those ahead of or
-  // equal to the cut block.
+// Writes a row's mask, kept-block list and count: the first m blocks of
+// (score desc, id asc), i.e. those ahead of or equal to the cut block.
+template <int KPL>
+__device__ __forceinline__ void emit_row(const double (&s)[KPL], int nb, int m, const Cut& cut,
+                                         uint8_t* __restrict__ mrow, int32_t* __restrict__ count_out,
+                                         int32_t* __restrict__ kvrow, WaveScratch& ws, int lane) {
   uint64_t mine = 0;  // lane k < KPL holds the kept bits of blocks 64k .. 64k+63
   int base = 0;
 #pragma unroll
@@ -556,23 +581,28 @@ __global__ __launch_bounds__(64 * kRowWaves, KPL > 12 ? 3 : 4) void select_kerne
                                                                    int64_t nrows, double p, int k_min,
                                                                    uint8_t* __restrict__ mask,
                                                                    int32_t* __restrict__ counts,
-                                                                   int32_t* __restrict__ kv_idx) {
+                                                                   int32_t* __restrict__ kv_idx,
+                                                                   RowCut* __restrict__ cuts) {
   __shared__ WaveScratch wsa[kRowWaves];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t row = (int64_t)blockIdx.x * kRowWaves + wave;
   if (row >= nrows) return;
   select_row<KPL>(scores + row * nb, nb, p, k_min, mask + row * nb, counts + row, kv_idx ? kv_idx + row * nb : nullptr,
-                  wsa[wave], lane);
+                  wsa[wave], lane, -1, cuts ? cuts + row : nullptr);
 }
 
 // Slack-aware augmentation, second pass: a row of a head with extra[h] > 0
-// blocks keeps the first min(nb, counts + extra) blocks of the same order
-// (the scores are those of the first pass); other rows are left as they are.
+// keeps the first min(nb, counts + extra) blocks of the same order (the
+// scores are those of the first pass); other rows are left as they are. The
+// first pass recorded each row's last kept block, so the blocks to add are
+// the first `extra` of those ranked after it: a count selection among them
+// alone, with no probabilities (the order is the scores').
 template <int KPL>
 __global__ __launch_bounds__(64 * kRowWaves, KPL > 12 ? 3 : 4) void augment_kernel(
     const double* __restrict__ scores, int nb, int64_t nrows, const int32_t* __restrict__ extra,
-    uint8_t* __restrict__ mask, int32_t* __restrict__ counts, int32_t* __restrict__ kv_idx) {
+    const RowCut* __restrict__ cuts, uint8_t* __restrict__ mask, int32_t* __restrict__ counts,
+    int32_t* __restrict__ kv_idx) {
   __shared__ WaveScratch wsa[kRowWaves];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -580,10 +610,47 @@ __global__ __launch_bounds__(64 * kRowWaves, KPL > 12 ? 3 : 4) void augment_kern
   if (row >= nrows) return;
   const int e = __builtin_amdgcn_readfirstlane(extra[row / nb]);
   if (e <= 0) return;
-  const int m0 = __builtin_amdgcn_readfirstlane(counts[row]);
-  const int m = (int)min((int64_t)nb, (int64_t)max(m0, 0) + e);
-  select_row<KPL>(scores + row * nb, nb, 0.0, 0, mask + row * nb, counts + row, kv_idx ? kv_idx + row * nb : nullptr,
-                  wsa[wave], lane, m);
+  const int m0 = min(max(__builtin_amdgcn_readfirstlane(counts[row]), 0), nb);
+  if (m0 >= nb) return;
+  const double s_cut = cuts[row].s;
+  const int j_cut = __builtin_amdgcn_readfirstlane(cuts[row].j);
+  const double* srow = scores + row * nb;
+  double s[KPL];
+  uint64_t F[KPL];
+  uint32_t cand = 0;
+  double cmax = -1.0e308, cmin = 1.0e308;
+#pragma unroll
+  for (int k = 0; k < KPL; ++k) {
+    const int j = lane + 64 * k;
+    F[k] = 0ull;
+    s[k] = -1.0e308;
+    if (j < nb) {
+      s[k] = srow[j];
+      if (s[k] < s_cut || (s[k] == s_cut && j > j_cut)) {
+        cand |= 1u << k;
+        cmax = fmax(cmax, s[k]);
+        cmin = fmin(cmin, s[k]);
+      }
+    }
+  }
+  int ncand = 0;
+#pragma unroll
+  for (int k = 0; k < KPL; ++k) ncand += __popcll(__ballot((cand >> k) & 1u));
+  const int add = min(e, ncand);
+  const int m = m0 + add;
+  Cut cut;
+  cut.s = s_cut;
+  cut.j = j_cut;
+  cut.rank = m0;
+  if (add > 0 && add < ncand) {
+    cut = select_cut<KPL>(s, F, cand, ncand, wave_min(cmin), wave_max(cmax), 0.0, false, (uint64_t)add, wsa[wave],
+                          lane);
+  } else if (add > 0) {
+    cut.s = -1.0e308;  // every candidate joins: the row keeps all its blocks
+    cut.j = nb;
+  }
+  emit_row<KPL>(s, nb, m >= nb ? nb : m, cut, mask + row * nb, counts + row, kv_idx ? kv_idx + row * nb : nullptr,
+                wsa[wave], lane);
 }
 
 // Slack-aware augmentation, budget (one workgroup): S_h = kept blocks of head
@@ -649,7 +716,7 @@ hipError_t launch_select(const RouteArgs& a, int nb, const double* scores) {
   const int64_t nrows = (int64_t)a.batch * a.heads * nb;
   const dim3 grid((unsigned)((nrows + kRowWaves - 1) / kRowWaves));
   hipLaunchKernelGGL(select_kernel<KPL>, grid, dim3(64 * kRowWaves), 0, a.stream, scores, nb, nrows, a.p, a.k_min,
-                     a.mask, a.counts, a.kv_idx);
+                     a.mask, a.counts, a.kv_idx, a.rank_of ? reinterpret_cast<RowCut*>(a.row_cuts) : nullptr);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !a.rank_of) return e;
   hipLaunchKernelGGL(sasa_budget_kernel, dim3(1), dim3(1024), 0, a.stream, a.counts, a.batch * a.heads, nb, a.rank_of,
@@ -657,7 +724,7 @@ hipError_t launch_select(const RouteArgs& a, int nb, const double* scores) {
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(augment_kernel<KPL>, grid, dim3(64 * kRowWaves), 0, a.stream, scores, nb, nrows, a.extra_head,
-                     a.mask, a.counts, a.kv_idx);
+                     reinterpret_cast<const RowCut*>(a.row_cuts), a.mask, a.counts, a.kv_idx);
   return hipGetLastError();
 }
 
@@ -682,7 +749,8 @@ size_t route_workspace_bytes(int batch, int heads, int nb) {
 }
 
 size_t route_sasa_workspace_bytes(int batch, int heads, int nb) {
-  return route_workspace_bytes(batch, heads, nb) + (((size_t)batch * heads * 4 + 255) & ~(size_t)255);
+  return route_workspace_bytes(batch, heads, nb) + (((size_t)batch * heads * 4 + 255) & ~(size_t)255) +
+         (((size_t)batch * heads * nb * sizeof(RowCut) + 255) & ~(size_t)255);
 }
 
 hipError_t launch_route(const RouteArgs& a) {
@@ -696,7 +764,10 @@ hipError_t launch_route(const RouteArgs& a) {
   double* kbar = reinterpret_cast<double*>(base + w.means);
   double* scores = reinterpret_cast<double*>(base + 2 * w.means);
   RouteArgs args = a;
-  if (a.rank_of) args.extra_head = reinterpret_cast<int32_t*>(base + 2 * w.means + w.scores);
+  if (a.rank_of) {
+    args.extra_head = reinterpret_cast<int32_t*>(base + 2 * w.means + w.scores);
+    args.row_cuts = base + 2 * w.means + w.scores + (((size_t)bhs * 4 + 255) & ~(size_t)255);
+  }
   hipLaunchKernelGGL(pool_kernel, dim3(padded_blocks(g.nb) / kPoolBlocks, bhs), dim3(kPoolThreads), 0, a.stream,
                      reinterpret_cast<const uint16_t*>(a.Q), reinterpret_cast<const uint16_t*>(a.K), a.heads,
                      a.stride_b, a.stride_h, a.stride_n, g, qbar, kbar);

@@ -229,7 +229,8 @@ def test_fp8_sizes_and_argument_errors():
 
 def test_route_sasa_sizes_and_argument_errors():
     d = desc()
-    assert fva.fva_route_sasa_workspace_size(d, T720) == fva.fva_route_workspace_size(d, T720) + 256  # 40 int32
+    # 40 int32 extra-block counts, then one 16-byte cut record per routed row (40 x 660)
+    assert fva.fva_route_sasa_workspace_size(d, T720) == fva.fva_route_workspace_size(d, T720) + 256 + 40 * 660 * 16
     L = fva.lib
     R = lambda rank_of=FAKE, n=8, n1=0.8, n2=0.07, ws=FAKE, wsb=1 << 40, extra=None: L.fva_route_sasa(
         FAKE, FAKE, ctypes.byref(d), 0.9, 4, ctypes.byref(T720.c()), rank_of, n, n1, n2, FAKE, FAKE, None, extra,
