@@ -20,14 +20,19 @@ Readings taken here (the paper leaves them open):
   min(nb, m + e_r) blocks of that order;
 * workloads are computed from exact integer sums: with S_h the sum of
   counts over the head's rows, L_h = S_h / nb, S_r = sum of S_h over the
-  rank, and the trigger and budget are evaluated in fp64 as
-      (S_max - S_r) > n2 * S_max,
-      e_r = floor((n1 * (S_max - S_r)) / (nb * H_r)),
-  the same expressions (in the same order) as the GPU path, so both sides
-  take the same integer decisions.
+  rank, and D_r = S_max - S_r. The trigger and the budget are decided in
+  exact rational arithmetic on the values n1 and n2 hold:
+      D_r > n2 * S_max,
+      e_r = floor(n1 * D_r / (nb * H_r)).
+  A kernel that evaluates them in floating point can decide otherwise only
+  when one of the two exact quantities lies within its rounding of the
+  boundary (D_r = n2 * S_max, or an integer quotient); boundary_ranks names
+  those ranks and the values either decision gives.
 
 Test infrastructure only; nothing here is shared with the GPU library.
 """
+
+from fractions import Fraction
 
 import numpy as np
 
@@ -45,6 +50,13 @@ def rank_loads(counts: np.ndarray, rank_of: np.ndarray, n_ranks: int):
     return S_r, H_r
 
 
+def _exact_decision(D: int, S_max: int, H: int, nb: int, n1: float, n2: float):
+    """(trigger fired, floor quotient, trigger margin, quotient) of one rank, exact."""
+    margin = Fraction(D) - Fraction(n2) * S_max
+    q = Fraction(n1) * D / (nb * H)
+    return margin > 0, int(q // 1), margin, q
+
+
 def sasa_extras(counts, rank_of, n_ranks: int, n1: float, n2: float):
     """Extra blocks per row for every rank (int64 [n_ranks]) and the per-rank figures.
 
@@ -58,11 +70,11 @@ def sasa_extras(counts, rank_of, n_ranks: int, n1: float, n2: float):
     extra = np.zeros(n_ranks, dtype=np.int64)
     fired = np.zeros(n_ranks, dtype=bool)
     for r in range(n_ranks):
-        D = S_max - int(S_r[r])
-        if H_r[r] == 0 or not (float(D) > float(n2) * float(S_max)):
+        if H_r[r] == 0:
             continue
-        fired[r] = True
-        extra[r] = int(np.floor((float(n1) * float(D)) / float(nb * int(H_r[r]))))
+        fire, e, _, _ = _exact_decision(S_max - int(S_r[r]), S_max, int(H_r[r]), nb, n1, n2)
+        fired[r] = fire
+        extra[r] = e if fire else 0
     info = {
         "L_r": S_r / nb,
         "dL_r": (S_max - S_r) / nb,
@@ -73,20 +85,58 @@ def sasa_extras(counts, rank_of, n_ranks: int, n1: float, n2: float):
     return extra, info
 
 
+def boundary_ranks(counts, rank_of, n_ranks: int, n1: float, n2: float, rel: float = 2.0**-48):
+    """Ranks whose decision sits at a boundary, and the extras either side gives.
+
+    A rank is at a boundary when its trigger margin D_r - n2 * S_max, or the
+    distance of its quotient n1 * D_r / (nb * H_r) to the nearest integer,
+    is within `rel` of the quantities involved (a few units of fp64
+    rounding). Returns {rank: set of acceptable extra values}; ranks not in
+    the dict have exactly one acceptable value, the exact one.
+    """
+    counts = np.asarray(counts, dtype=np.int64)
+    nb = counts.shape[1]
+    S_r, H_r = rank_loads(counts, rank_of, n_ranks)
+    S_max = int(S_r.max()) if n_ranks > 0 else 0
+    out = {}
+    for r in range(n_ranks):
+        if H_r[r] == 0:
+            continue
+        D = S_max - int(S_r[r])
+        fire, e, margin, q = _exact_decision(D, S_max, int(H_r[r]), nb, n1, n2)
+        fires = {fire}
+        if abs(margin) <= Fraction(rel) * max(D, Fraction(n2) * S_max, 1):
+            fires = {True, False}
+        floors = {e}
+        near = round(q)
+        if abs(q - near) <= Fraction(rel) * max(q, 1):
+            floors = {max(near - 1, 0), near}
+        ok = {f if fr else 0 for fr in fires for f in floors}
+        if len(ok) > 1:
+            out[r] = ok
+    return out
+
+
+def augment_with(order: np.ndarray, counts: np.ndarray, rank_of, extra):
+    """(mask, counts) when every row of rank r keeps min(nb, m + extra[r]) blocks of its order."""
+    order = np.asarray(order)
+    counts = np.asarray(counts, dtype=np.int64)
+    heads, nb = counts.shape
+    rank_of = np.asarray(rank_of, dtype=np.int64)
+    new_counts = np.minimum(nb, counts + np.asarray(extra, dtype=np.int64)[rank_of][:, None])
+    mask = np.zeros((heads, nb, nb), dtype=np.uint8)
+    for h in range(heads):
+        for i in range(nb):
+            mask[h, i, order[h, i, : new_counts[h, i]]] = 1
+    return mask, new_counts
+
+
 def sasa_augment(order: np.ndarray, counts: np.ndarray, rank_of, n_ranks: int, n1: float, n2: float):
     """Augmented (mask, counts) of every head: first min(nb, m + e_r) blocks of each row's order.
 
     order: int [heads, nb, nb], the routing order of every row (score
     descending, ties to the lower id), as route_ref returns it.
     """
-    order = np.asarray(order)
-    counts = np.asarray(counts, dtype=np.int64)
-    heads, nb = counts.shape
     extra, info = sasa_extras(counts, rank_of, n_ranks, n1, n2)
-    rank_of = np.asarray(rank_of, dtype=np.int64)
-    new_counts = np.minimum(nb, counts + extra[rank_of][:, None])
-    mask = np.zeros((heads, nb, nb), dtype=np.uint8)
-    for h in range(heads):
-        for i in range(nb):
-            mask[h, i, order[h, i, : new_counts[h, i]]] = 1
+    mask, new_counts = augment_with(order, counts, rank_of, extra)
     return mask, new_counts, extra, info

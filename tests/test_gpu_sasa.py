@@ -1,10 +1,13 @@
 """GPU parity of slack-aware augmentation (fva_route_sasa) against the oracle.
 
 Integer work end to end: the routing order and first-pass counts are those
-of fva_route (bit-exact against the oracle on these workloads), and the
-budget decisions are evaluated from exact integer sums with the same fp64
-expressions on both sides, so the augmented mask, counts, kept lists and the
-per-rank extra blocks must equal oracle.sasa.sasa_augment bit for bit.
+of fva_route (bit-exact against the oracle on these workloads). The oracle
+decides each rank's trigger and extra blocks in exact rational arithmetic;
+the kernel's fp64 evaluation must give the same value, except at a rank
+that oracle.sasa.boundary_ranks names (an exact quantity within fp64
+rounding of its boundary), where either side's value is accepted and the
+mask is then checked for the kernel's value. The augmented mask, counts and
+kept lists must equal the oracle's bit for bit.
 """
 
 import numpy as np
@@ -12,7 +15,7 @@ import pytest
 
 import synth
 from oracle import route_ref
-from oracle.sasa import rank_loads, sasa_augment
+from oracle.sasa import augment_with, boundary_ranks, rank_loads, sasa_extras
 
 from _gpu_util import custom_config, f64, geometry_of, lib, log, tiling_of, to_dev, torch_mod, workload
 
@@ -30,6 +33,23 @@ def run_sasa(Qb, Kb, cfg, rank_of, n_ranks, n1, n2):
             plain[1].cpu().numpy()[0])
 
 
+def accepted_extras(got, counts, rank_of, n_ranks, n1, n2):
+    """The kernel's per-rank extras, checked against the oracle's exact ones.
+
+    Equal, or (at a boundary rank) one of the values either decision gives.
+    Returns the extras to build the reference mask from.
+    """
+    e_ref, _ = sasa_extras(counts, rank_of, n_ranks, n1, n2)
+    bound = boundary_ranks(counts, rank_of, n_ranks, n1, n2)
+    got = np.asarray(got, dtype=np.int64)
+    for r in range(n_ranks):
+        assert int(got[r]) in bound.get(r, {int(e_ref[r])}), (r, got[r], e_ref[r], bound.get(r))
+    if bound:
+        log(f"[sasa] boundary ranks {sorted(bound)}: kernel {[int(got[r]) for r in sorted(bound)]}, "
+            f"exact {[int(e_ref[r]) for r in sorted(bound)]}")
+    return got
+
+
 def check(name, Qb, Kb, cfg, rank_of, n_ranks, n1=0.8, n2=0.07):
     geo = geometry_of(cfg)
     mask, counts, kv, extra, counts0 = run_sasa(Qb, Kb, cfg, rank_of, n_ranks, n1, n2)
@@ -38,14 +58,14 @@ def check(name, Qb, Kb, cfg, rank_of, n_ranks, n1=0.8, n2=0.07):
     rank_of = np.asarray(rank_of)
     valid = (rank_of >= 0) & (rank_of < n_ranks)
     keep = np.nonzero(valid)[0]  # heads without a rank take no part and stay as routed
-    _, c_sub, e_ref, _ = sasa_augment(ref["order"][keep], ref["counts"][keep], rank_of[keep], n_ranks, n1, n2)
+    e_use = accepted_extras(extra[:n_ranks], ref["counts"][keep], rank_of[keep], n_ranks, n1, n2)
+    _, c_sub = augment_with(ref["order"][keep], ref["counts"][keep], rank_of[keep], e_use)
     c_ref = ref["counts"].copy()
     c_ref[keep] = c_sub
     m_ref = np.zeros_like(mask)
     for h in range(mask.shape[0]):
         for i in range(geo.nb):
             m_ref[h, i, ref["order"][h, i, : c_ref[h, i]]] = 1
-    assert np.array_equal(extra[:n_ranks], e_ref), (extra, e_ref)
     assert np.array_equal(counts, c_ref)
     assert np.array_equal(mask, m_ref)
     for h in range(mask.shape[0]):
@@ -104,11 +124,11 @@ def test_sasa_batch_two():
     torch.cuda.synchronize()
     order = np.concatenate([route_ref(f64(Qb[b]), f64(Kb[b]), cfg.p, cfg.k_min, geo)["order"] for b in range(2)])
     c0 = np.concatenate([route_ref(f64(Qb[b]), f64(Kb[b]), cfg.p, cfg.k_min, geo)["counts"] for b in range(2)])
-    m_ref, c_ref, e_ref, _ = sasa_augment(order, c0, rank_of, 3, 0.8, 0.0)
-    assert np.array_equal(extra.cpu().numpy(), e_ref)
+    e_use = accepted_extras(extra.cpu().numpy(), c0, rank_of, 3, 0.8, 0.0)
+    m_ref, c_ref = augment_with(order, c0, rank_of, e_use)
     assert np.array_equal(counts.cpu().numpy().reshape(6, -1), c_ref)
     assert np.array_equal(mask.cpu().numpy().reshape(6, geo.nb, geo.nb), m_ref)
-    log(f"[sasa] batch 2: extra per rank {e_ref.tolist()}")
+    log(f"[sasa] batch 2: extra per rank {e_use.tolist()}")
 
 
 def test_sasa_one_rank_per_head_and_max_ranks():
