@@ -285,13 +285,28 @@ __device__ Cut select_cut(const double (&s)[KPL], const uint64_t (&F)[KPL], uint
       const uint64_t wl = has ? ws.cw[lane] : 0ull;
       uint64_t ahead = 0;
       int rank = 0;
-#pragma unroll 4
-      for (int m = 0; m < ncand; ++m) {
-        const double sm = ws.cs[m];
-        const int jm = ws.cj[m];
-        const bool prec = sm > sl || (sm == sl && jm < jl);
-        ahead += prec ? ws.cw[m] : 0ull;
-        rank += prec ? 1 : 0;
+      // Eight candidates per step, read unconditionally (entries past ncand
+      // are masked, the arrays hold 64) and combined without branches, so
+      // the step's LDS reads are in flight together.
+      for (int m0 = 0; m0 < ncand; m0 += 8) {
+        double sm[8];
+        int jm[8];
+        uint64_t wm[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          sm[u] = ws.cs[m0 + u];
+          jm[u] = ws.cj[m0 + u];
+          wm[u] = ws.cw[m0 + u];
+        }
+        // keeps the weight reads unconditional (issued with the others)
+        asm volatile("" : "+v"(wm[0]), "+v"(wm[1]), "+v"(wm[2]), "+v"(wm[3]), "+v"(wm[4]), "+v"(wm[5]), "+v"(wm[6]),
+                     "+v"(wm[7]));
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const bool prec = (m0 + u < ncand) & ((sm[u] > sl) | ((sm[u] == sl) & (jm[u] < jl)));
+          ahead += prec ? wm[u] : 0ull;
+          rank += (int)prec;
+        }
       }
       const uint64_t before = W0 + ahead;
       uint64_t hit = __ballot(has && before < thr && before + wl >= thr);
