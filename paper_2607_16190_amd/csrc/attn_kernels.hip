@@ -368,6 +368,13 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) o[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   float mrow[2] = {-1.0e30f, -1.0e30f};
+  // Per row, the score above which the reference moves (mrow + 8 / c2 for
+  // bf16 P, mrow + 1 / c2 for E4M3 P) and the exponent offset (-mrow * c2,
+  // plus 7 for E4M3 P), both refreshed only when mrow moves.
+  const float move_ref = (F8 ? 1.0f : 8.0f) / P.c2;
+  constexpr float kPOffset = F8 ? 7.0f : 0.0f;
+  float thr[2] = {-1.0e30f, -1.0e30f};
+  float negm[2] = {0.f, 0.f};
   // Softmax denominators on the matrix unit: an extra O^T tile whose V^T
   // operand is all ones accumulates sum_k P[k] for every query row (all 16
   // rows of the tile hold it), rescaled together with O.
@@ -448,8 +455,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   // Online softmax over the half. Accumulator (t, r) of lane group g4 holds
   // key 64hb + 32*(t/2) + 8*g4 + 4*(t%2) + r; keys past nj are masked (in a
   // short half that covers every key of tiles 2 and 3).
-  auto softmax_phase = [&](int hb, bool short_half, int nj, f32x4 (&s)[4][2], bf16x8 (&pb)[2][2],
-                           float (&negm)[2]) {
+  auto softmax_phase = [&](int hb, bool short_half, int nj, f32x4 (&s)[4][2], bf16x8 (&pb)[2][2]) {
     if (nj < 64 * hb + 64) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
@@ -478,13 +484,11 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
     // the final O / l is unchanged. A row's max is the max over its four
     // lane groups, all in this wave: when no lane's own max passes the
     // threshold, no row's does, and the cross-lane max is skipped.
-    const bool want0 = (mx[0] - mrow[0]) * P.c2 > 8.0f;
-    const bool want1 = (mx[1] - mrow[1]) * P.c2 > 8.0f;
-    if (__ballot(want0 || want1)) {
+    if (__ballot(mx[0] > thr[0] || mx[1] > thr[1])) {
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
         const float rmx = row_max4(mx[nt]);
-        const bool grow = (rmx - mrow[nt]) * P.c2 > 8.0f;
+        const bool grow = rmx > thr[nt];
         const float mref = grow ? rmx : mrow[nt];
         const float alpha = grow ? __builtin_amdgcn_exp2f((mrow[nt] - mref) * P.c2) : 1.0f;
         mrow[nt] = mref;
@@ -492,11 +496,11 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
 #pragma unroll
           for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha;
           lsum[nt] *= alpha;
+          thr[nt] = mrow[nt] + move_ref;
+          negm[nt] = -mrow[nt] * P.c2;
         }
       }
     }
-    negm[0] = -mrow[0] * P.c2;
-    negm[1] = -mrow[1] * P.c2;
     // The first 32 keys only: the exponentials of the second 32 are taken
     // inside the PV phase, under the products of the first.
 #pragma unroll
@@ -631,21 +635,19 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
         mx[1] = fmaxf(mx[1], s[t][1][r]);
       }
     }
-    const bool want0 = (mx[0] - mrow[0]) * P.c2 > 1.0f;
-    const bool want1 = (mx[1] - mrow[1]) * P.c2 > 1.0f;
-    if (__ballot(want0 || want1)) {
+    if (__ballot(mx[0] > thr[0] || mx[1] > thr[1])) {
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
         const float rmx = row_max4(mx[nt]);
-        const float dist = (rmx - mrow[nt]) * P.c2;
-        const bool grow = dist > 1.0f;
+        const bool grow = rmx > thr[nt];
         float alpha = 1.0f;
         if (hb == 0) {
           const float mref = grow ? rmx : mrow[nt];
           alpha = grow ? __builtin_amdgcn_exp2f((mrow[nt] - mref) * P.c2) : 1.0f;
           mrow[nt] = mref;
         } else if (grow) {
-          const int k = (int)ceilf(dist - 1.0f);  // >= 1
+          // a whole number of powers of two, at least one
+          const int k = max((int)ceilf((rmx - mrow[nt]) * P.c2 - 1.0f), 1);
           kb[nt] = k;
           mrow[nt] += (float)k / P.c2;
           alpha = k > 126 ? 0.0f : __uint_as_float((uint32_t)(127 - k) << 23);
@@ -654,10 +656,11 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
 #pragma unroll
           for (int mt = 0; mt < 8; ++mt) o[mt][nt] *= alpha;
           lsum[nt] *= alpha;
+          thr[nt] = mrow[nt] + move_ref;
+          negm[nt] = kPOffset - mrow[nt] * P.c2;
         }
       }
     }
-    const float negm[2] = {7.0f - mrow[0] * P.c2, 7.0f - mrow[1] * P.c2};
     auto tile = [&](auto t_c) {
       constexpr int t = decltype(t_c)::value;
 #pragma unroll
@@ -739,7 +742,6 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
       const bool short_half = hb == 1 && ng == 3;
       f32x4 s[4][2];
       bf16x8 pb[2][2];
-      float negm[2];
       if (active && run) s_phase(hb, short_half, s);
       if (hb == 0) {
         // record of block c + 1 and the id of block c + 2 (clamped to the list)
@@ -758,7 +760,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
           }
         }
       }
-      if (active && run) softmax_phase(hb, short_half, nj, s, pb, negm);
+      if (active && run) softmax_phase(hb, short_half, nj, s, pb);
       if (hb == 0) {
         // The prefetched scalars have landed long ago; waiting for them here,
         // where no LDS read is in flight, keeps the PV fragment waits exact.
