@@ -406,14 +406,35 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
     if constexpr (F8) issue_v8_tile(V8h, jc, Vs);
   }
 
+  // LDS addresses of the lane's fragments, formed once per item: the
+  // swizzled lane part differs per V channel tile mt and per K head-dim step
+  // ks, and the rest (key group, K row tile) is an immediate offset. In the
+  // bf16 kernel they are opaque to the compiler, which would otherwise
+  // re-add the lane parts at every read.
+  uint32_t vaddr[8], kaddr[4];
+  {
+    const uint32_t vbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)Vs;
+    const uint32_t kbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)Ks;
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) vaddr[mt] = vbase + (uint32_t)(vrow + 8 * (4 * (mt ^ vsw) + tq));
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) kaddr[ks] = kbase + (uint32_t)(l16 * kRowBytes + 16 * ((4 * ks + g4) ^ l16));
+    if constexpr (!F8) {  // (the FP8 kernel has no registers to spare for them)
+      asm volatile("" : "+v"(vaddr[0]), "+v"(vaddr[1]), "+v"(vaddr[2]), "+v"(vaddr[3]), "+v"(vaddr[4]),
+                   "+v"(vaddr[5]), "+v"(vaddr[6]), "+v"(vaddr[7]));
+      asm volatile("" : "+v"(kaddr[0]), "+v"(kaddr[1]), "+v"(kaddr[2]), "+v"(kaddr[3]));
+    }
+  }
+  typedef __attribute__((address_space(3))) unsigned char lds_u8;
+  typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
   auto vfrag = [&](int kg, int mt) {
-    const unsigned char* vb = Vs + kg * 32 * kRowBytes + vrow + 8 * (4 * (mt ^ vsw) + tq);
-    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds_void*)vb);
-    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds_void*)(vb + 16 * kRowBytes));
+    lds_u8* vb = (lds_u8*)(uintptr_t)vaddr[mt] + kg * 32 * kRowBytes;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)vb);
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb + 16 * kRowBytes));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
   auto kfrag = [&](int mt, int ks) {
-    return *reinterpret_cast<const bf16x8*>(Ks + (mt * 16 + l16) * kRowBytes + 16 * ((4 * ks + g4) ^ l16));
+    return *(lds_bf16x8*)((lds_u8*)(uintptr_t)kaddr[ks] + mt * 16 * kRowBytes);
   };
 
   // One half of a block: S^T for its key groups (LDS tiles 4hb .. 4hb + 3),
