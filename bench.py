@@ -198,6 +198,103 @@ ROUTE_TRAFFIC = {
 }
 
 
+def extra_workloads(torch, fva, synth, dev, reps=3):
+    """The other two timed workloads, outside the timed region, as extra keys.
+
+    long: the 31x45x80 clip (111,600 tokens, nb 960) at p = 0.8, 0.9 and 0.95:
+    retained fraction, route and attention times (HIP events, mean of reps
+    after one warmup each).
+    720p_stress: 8 flat and 32 concentrated heads of the 720p shape: attention
+    time under the persistent scheduler and under the naive head-major grid,
+    and from one traced run of each the per-CU busy max/mean, the per-XCD
+    imbalance and the span (Eq. 2 with XCDs as ranks).
+    """
+    stream = torch.cuda.current_stream()
+    out = {}
+
+    def load(name):
+        cfg = synth.get_config(name)
+        log(f"[bench] extra workload {name}: generating {cfg.heads} heads x {cfg.N} tokens")
+        Qb, Kb, Vb = synth.gen_qkv(cfg)
+        up = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        q, k, v = up(Qb), up(Kb), up(Vb)
+        del Qb, Kb, Vb
+        tiling = fva.Tiling(*cfg.grid, *cfg.tile)
+        nb = fva.fva_num_blocks(tiling)
+        B, H = q.shape[0], q.shape[1]
+        bufs = dict(mask=torch.empty((B, H, nb, nb), dtype=torch.uint8, device=dev),
+                    counts=torch.empty((B, H, nb), dtype=torch.int32, device=dev),
+                    kv=torch.empty((B, H, nb, nb), dtype=torch.int32, device=dev),
+                    out=torch.empty_like(q),
+                    ws_r=torch.empty(fva.fva_route_workspace_size(fva._desc_of(q), tiling), dtype=torch.uint8,
+                                     device=dev),
+                    ws_a=torch.empty(fva.fva_attn_workspace_size(fva._desc_of(q), tiling), dtype=torch.uint8,
+                                     device=dev))
+        return cfg, tiling, nb, (q, k, v), bufs
+
+    def timed_pair(route_fn, attn_fn):
+        route_fn()
+        attn_fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        tr, ta = 0.0, 0.0
+        for _ in range(reps):
+            ev[0].record(stream)
+            route_fn()
+            ev[1].record(stream)
+            attn_fn()
+            ev[2].record(stream)
+            torch.cuda.synchronize()
+            tr += ev[0].elapsed_time(ev[1])
+            ta += ev[1].elapsed_time(ev[2])
+        return tr / reps, ta / reps
+
+    # long clip: retained fraction vs time over the p sweep
+    cfg, tiling, nb, (q, k, v), b = load("long")
+    sweep = []
+    for pp in (0.8, 0.9, 0.95):
+        route_fn = lambda: fva.fva_route(q, k, pp, cfg.k_min, tiling, out=(b["mask"], b["counts"], b["kv"]),
+                                         workspace=b["ws_r"])
+        attn_fn = lambda: fva.fva_attn(q, k, v, tiling, b["mask"], b["counts"], b["kv"], out=b["out"],
+                                       workspace=b["ws_a"])
+        t_r, t_a = timed_pair(route_fn, attn_fn)
+        kept = int(b["counts"].sum().item())
+        dense = 4.0 * q.shape[1] * float(cfg.N) ** 2 * 128
+        sweep.append({"p": pp, "retained_fraction": round(kept / (q.shape[1] * nb * nb), 4),
+                      "route_us": round(t_r * 1e3, 1), "attn_ms": round(t_a, 3),
+                      "kept_tile_TFLOPS": round(4.0 * 128**3 * kept / (t_a / 1e3) / 1e12, 1),
+                      "dense_equiv_TFLOPS": round(dense / ((t_r + t_a) / 1e3) / 1e12, 1)})
+        log(f"[bench] long p={pp}: {sweep[-1]}")
+    out["long_p_sweep"] = {"workload": f"long: {q.shape[1]} heads, 31x45x80 = {cfg.N} tokens, tile 2x8x8, nb={nb}, "
+                                       f"k_min={cfg.k_min}", "reps": reps, "points": sweep}
+    del q, k, v, b
+    torch.cuda.empty_cache()
+
+    # stress: persistent scheduler against the naive head-major grid
+    cfg, tiling, nb, (q, k, v), b = load("720p_stress")
+    fva.fva_route(q, k, cfg.p, cfg.k_min, tiling, out=(b["mask"], b["counts"], b["kv"]), workspace=b["ws_r"])
+    c_np = b["counts"].cpu().numpy()
+    res = {"workload": f"720p_stress: {q.shape[1]} heads (8 at alpha 0.3, 32 at alpha 5), 21x45x80, tile 2x8x8, "
+                       f"nb={nb}, p={cfg.p}, k_min={cfg.k_min}",
+           "retained_fraction": round(float(c_np.sum()) / (q.shape[1] * nb * nb), 4)}
+    tw = fva.fva_trace_words(fva._desc_of(q), tiling)
+    trace = torch.zeros(tw, dtype=torch.int64, device=dev)
+    for name, fl in (("persistent", fva.FVA_SCHED_PERSISTENT), ("naive", fva.FVA_SCHED_NAIVE)):
+        attn_fn = lambda: fva.fva_attn(q, k, v, tiling, b["mask"], b["counts"], b["kv"], flags=fl, out=b["out"],
+                                       workspace=b["ws_a"])
+        _, t_a = timed_pair(lambda: None, attn_fn)
+        trace.zero_()
+        fva.fva_attn(q, k, v, tiling, b["mask"], b["counts"], b["kv"], flags=fl | fva.FVA_TRACE, out=b["out"],
+                     workspace=b["ws_a"], trace=trace)
+        torch.cuda.synchronize()
+        res[name] = {"attn_ms": round(t_a, 3), **imbalance(trace.cpu().numpy(), c_np)}
+        log(f"[bench] stress {name}: {res[name]}")
+    out["stress_scheduler"] = res
+    del q, k, v, b, trace
+    torch.cuda.empty_cache()
+    return out
+
+
 def gemm_ceiling(torch, n=8192, reps=10):
     """bf16 matrix ceiling of this device as the vendor GEMM reaches it: an
     n x n x n torch.matmul (hipBLASLt), HIP events, mean of reps after two
