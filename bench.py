@@ -177,23 +177,23 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "16e4983c728f3bf3",
+    "source_digest": "f5708f4d3f7424be",
     "bytes": {
-        "720p": ((114348982 + 112026495) // 2 * 2 + 757142) * 1024,
-        "720p-hilbert": ((77310631 + 77281792) // 2 * 2 + 757198) * 1024,
-        "720p-fp8v": ((71290242 + 71052433) // 2 * 2 + 758060) * 1024,
-        "720p-hilbert-fp8v": ((67000790 + 66835179) // 2 * 2 + 757989) * 1024,
+        "720p": ((107668438 + 108084709) // 2 * 2 + 759717) * 1024,
+        "720p-hilbert": ((81189571 + 80863710) // 2 * 2 + 759861) * 1024,
+        "720p-fp8v": ((69228639 + 69429658) // 2 * 2 + 758040) * 1024,
+        "720p-hilbert-fp8v": ((68103201 + 67970834) // 2 * 2 + 758024) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "245cb60d8727db05",
+    "source_digest": "75b7b87c55e1e764",
     "bytes": {
-        "720p": ((756188 + 29439 + 68209) * 2 + 53760 + 138821 + 49287) * 1024,
-        "720p-hilbert": ((756159 + 25783 + 55008) * 2 + 47360 + 112513 + 39990) * 1024,
-        "720p-fp8v": ((756187 + 29550 + 68208) * 2 + 53760 + 138789 + 49287) * 1024,
-        "720p-hilbert-fp8v": ((756156 + 25871 + 55007) * 2 + 47360 + 112712 + 39990) * 1024,
+        "720p": ((756187 + 29583 + 68220) * 2 + 53760 + 139190 + 49285) * 1024,
+        "720p-hilbert": ((756157 + 25653 + 55021) * 2 + 47360 + 112515 + 39989) * 1024,
+        "720p-fp8v": ((756188 + 29446 + 68216) * 2 + 53760 + 139038 + 49286) * 1024,
+        "720p-hilbert-fp8v": ((756156 + 25592 + 55020) * 2 + 47360 + 112344 + 39989) * 1024,
     },
 }
 
