@@ -13,8 +13,9 @@
   tail on the full-size row sets). Bar, per element: |O - O'| <= that bound +
   1e-2, the error of the rest of the arithmetic (bf16 Q K^T products, fp32
   softmax and accumulation, bf16 output): the bf16 path, which does the same
-  arithmetic with bf16 instead of E4M3 probabilities, stays within 8.9e-3 of
-  the fp64 oracle on every case measured (largest of its parity cases). Over
+  arithmetic with bf16 instead of E4M3 probabilities, stays within 9.6e-3 of
+  the fp64 oracle on every case measured (largest of its parity cases: the
+  stress workload on Hilbert-curve blocks). Over
   all compared elements: mean |O - O'| <= 1e-3 + mean of
   sqrt(sum_k (c_k w_k)^2 (v_k - O')^2) (the spread of the rounding sum for
   independent errors).
@@ -44,7 +45,7 @@ from _gpu_util import (
 
 pytestmark = pytest.mark.gpu
 
-ALLOW_OWN = 1e-2  # the rest of the arithmetic; the bf16 path's largest measured error is 8.9e-3
+ALLOW_OWN = 1e-2  # the rest of the arithmetic; the bf16 path's largest measured error is 9.6e-3
 ALLOW_MEAN = 1e-3
 
 
