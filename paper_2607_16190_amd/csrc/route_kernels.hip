@@ -107,8 +107,13 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
           const int tok = fast ? tb + (j >> 4) * HW + ((j >> 1) & 7) * g.W + 4 * (j & 1)
                           : line ? tb + 4 * j : box_token(g, box, r);
           const int64_t off = base + (int64_t)tok * sn;
-          vq[jj] = *reinterpret_cast<const uint4*>(Q + off);
-          vk[jj] = *reinterpret_cast<const uint4*>(K + off);
+          // streaming loads: every byte of Q and K is read once here, and
+          // the caches are left to the score rows and to the attention's K/V
+          typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
+          const u32x4_nt lq = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(Q + off));
+          const u32x4_nt lk = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(K + off));
+          vq[jj] = make_uint4(lq.x, lq.y, lq.z, lq.w);
+          vk[jj] = make_uint4(lk.x, lk.y, lk.z, lk.w);
         } else {
           vq[jj] = make_uint4(0, 0, 0, 0);
           vk[jj] = make_uint4(0, 0, 0, 0);
