@@ -398,7 +398,7 @@ __device__ __forceinline__ void select_row(const double* __restrict__ srow, int 
   for (int k = 0; k < KPL; ++k) {
     const int j = lane + 64 * k;
     if (j < nb) {
-      s[k] = srow[j];
+      s[k] = __builtin_nontemporal_load(srow + j);  // each score row is read once
       valid |= 1u << k;
       vmax = fmax(vmax, s[k]);
       vmin = fmin(vmin, s[k]);
