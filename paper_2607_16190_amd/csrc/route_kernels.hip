@@ -5,10 +5,15 @@
 //                  per (b, h) and 8 consecutive blocks streams their rows of
 //                  Q and K once (sixteen lanes per 256-byte token row) and
 //                  writes the means as whole lines in MFMA operand order.
-// select_kernel -- for 16 query blocks of one (b, h): fp64 scores against
-//                  every key block, softmax, Top-p cut with the Top-k floor
-//                  (§2.1), then the mask row, the count and the ascending
-//                  kept-block list. One wavefront owns one row at a time.
+// score_kernel  -- for 16 query blocks of one (b, h): fp64 products of the
+//                  means against every key block on the fp64 matrix unit,
+//                  written as score rows.
+// select_kernel -- per score row (one wavefront each): softmax, Top-p cut
+//                  with the Top-k floor (§2.1), then the mask row, the count
+//                  and the ascending kept-block list.
+// sasa_budget_kernel, augment_kernel -- the slack-aware augmentation
+//                  (§3.3, Eq. 7-10, read over a head -> rank map): per-rank
+//                  budgets, then extra blocks appended in the same order.
 //
 // The Top-p cut never sorts the row. The probabilities are turned into
 // fixed-point masses F_j = round(P_j * 2^52), so every partial sum is exact
