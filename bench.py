@@ -179,21 +179,21 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 ATTN_TRAFFIC = {
     "source_digest": "f5708f4d3f7424be",
     "bytes": {
-        "720p": ((107668438 + 108084709) // 2 * 2 + 759717) * 1024,
-        "720p-hilbert": ((81189571 + 80863710) // 2 * 2 + 759861) * 1024,
-        "720p-fp8v": ((69228639 + 69429658) // 2 * 2 + 758040) * 1024,
-        "720p-hilbert-fp8v": ((68103201 + 67970834) // 2 * 2 + 758024) * 1024,
+        "720p": ((107432680 + 108789874) // 2 * 2 + 759707) * 1024,
+        "720p-hilbert": ((80858098 + 80368873) // 2 * 2 + 759873) * 1024,
+        "720p-fp8v": ((68823409 + 69244199) // 2 * 2 + 758062) * 1024,
+        "720p-hilbert-fp8v": ((68236731 + 67927669) // 2 * 2 + 757993) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "75b7b87c55e1e764",
+    "source_digest": "a0c3f570f89950fd",
     "bytes": {
-        "720p": ((756187 + 29583 + 68220) * 2 + 53760 + 139190 + 49285) * 1024,
-        "720p-hilbert": ((756157 + 25653 + 55021) * 2 + 47360 + 112515 + 39989) * 1024,
-        "720p-fp8v": ((756188 + 29446 + 68216) * 2 + 53760 + 139038 + 49286) * 1024,
-        "720p-hilbert-fp8v": ((756156 + 25592 + 55020) * 2 + 47360 + 112344 + 39989) * 1024,
+        "720p": ((756174 + 31614 + 71523) * 2 + 53760 + 137666 + 49285) * 1024,
+        "720p-hilbert": ((756150 + 26909 + 58235) * 2 + 47360 + 111423 + 39989) * 1024,
+        "720p-fp8v": ((756174 + 31509 + 71596) * 2 + 53760 + 137751 + 49285) * 1024,
+        "720p-hilbert-fp8v": ((756149 + 26960 + 58236) * 2 + 47360 + 111588 + 39989) * 1024,
     },
 }
 
