@@ -510,7 +510,7 @@ __device__ __forceinline__ void emit_row(const double (&s)[KPL], int nb, int m, 
 }
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
-constexpr int kScoreThreads = 256;  // 4 waves; two workgroups per CU overlap their start-up loads
+constexpr int kScoreThreads = 256;  // 4 waves; several workgroups per CU overlap their tile loads
 constexpr int kRowWaves = 4;        // rows (one per wavefront) per select workgroup
 
 // Workgroup n of a 1-D grid runs on XCD n % 8. Logical workgroups are dealt
@@ -527,7 +527,7 @@ __device__ __forceinline__ int xcd_contiguous(int n, int total) {
 // step k, so the 32 steps sum the full 128-dim dot product. Wave w takes key
 // tiles w, w+4, ... The grid is one-dimensional over (head, query tile); the
 // products go to a row-major [B*H*nb, nb] fp64 buffer.
-__global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __restrict__ qbar,
+__global__ __launch_bounds__(kScoreThreads, 3) void score_kernel(const double* __restrict__ qbar,
                                                              const double* __restrict__ kbar, int nb,
                                                              double* __restrict__ scores) {
   const int ntq = (nb + kSelRows - 1) / kSelRows;
@@ -559,7 +559,6 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __re
   }
   const double* kb = kbar + head_off + 2 * lane;
   double* srow = scores + ((int64_t)bh * nb + i0) * nb;
-  // A wave's next key tile loads while its current one multiplies.
   auto load_tile = [&](int t, double (&kk)[32]) {
     const double* kr = kb + (int64_t)t * 16 * kHeadDim;
 #pragma unroll
@@ -584,19 +583,13 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const double* __re
       }
     }
   };
-  double ka[32], kn[32];
-  int t = wave;
-  if (t < ntiles) load_tile(t, ka);
-  while (t < ntiles) {
-    const int tn = t + nwaves;
-    if (tn < ntiles) load_tile(tn, kn);
+  // One key tile in registers at a time (104 VGPRs, so four waves per SIMD):
+  // they hide each other's tile loads better than two waves that each
+  // double-buffer their tiles.
+  double ka[32];
+  for (int t = wave; t < ntiles; t += nwaves) {
+    load_tile(t, ka);
     score_tile(t, ka);
-    t = tn;
-    if (t >= ntiles) break;
-    const int tn2 = t + nwaves;
-    if (tn2 < ntiles) load_tile(tn2, ka);
-    score_tile(t, kn);
-    t = tn2;
   }
 }
 
