@@ -179,21 +179,21 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 ATTN_TRAFFIC = {
     "source_digest": "f5708f4d3f7424be",
     "bytes": {
-        "720p": ((107432680 + 108789874) // 2 * 2 + 759707) * 1024,
-        "720p-hilbert": ((80858098 + 80368873) // 2 * 2 + 759873) * 1024,
-        "720p-fp8v": ((68823409 + 69244199) // 2 * 2 + 758062) * 1024,
-        "720p-hilbert-fp8v": ((68236731 + 67927669) // 2 * 2 + 757993) * 1024,
+        "720p": ((107809152 + 107751492) // 2 * 2 + 759685) * 1024,
+        "720p-hilbert": ((80433327 + 80481098) // 2 * 2 + 759862) * 1024,
+        "720p-fp8v": ((69018673 + 69564284) // 2 * 2 + 758044) * 1024,
+        "720p-hilbert-fp8v": ((67994091 + 67917736) // 2 * 2 + 757982) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "a0c3f570f89950fd",
+    "source_digest": "cd3c88b9dc4dee67",
     "bytes": {
-        "720p": ((756174 + 31614 + 71523) * 2 + 53760 + 137666 + 49285) * 1024,
-        "720p-hilbert": ((756150 + 26909 + 58235) * 2 + 47360 + 111423 + 39989) * 1024,
-        "720p-fp8v": ((756174 + 31509 + 71596) * 2 + 53760 + 137751 + 49285) * 1024,
-        "720p-hilbert-fp8v": ((756149 + 26960 + 58236) * 2 + 47360 + 111588 + 39989) * 1024,
+        "720p": ((756174 + 29278 + 71517) * 2 + 53760 + 142451 + 49285) * 1024,
+        "720p-hilbert": ((756151 + 25318 + 58247) * 2 + 47360 + 117177 + 39989) * 1024,
+        "720p-fp8v": ((756173 + 29322 + 71553) * 2 + 53760 + 142328 + 49285) * 1024,
+        "720p-hilbert-fp8v": ((756149 + 25310 + 58231) * 2 + 47360 + 117559 + 39989) * 1024,
     },
 }
 
