@@ -83,6 +83,15 @@ typedef struct fva_qkv_desc {
 #define FVA_SCHED_PERSISTENT 0u /* persistent grid pulling (head, query-block) items, heaviest first */
 #define FVA_SCHED_NAIVE 1u      /* one workgroup per item in head-major order (same kernel body) */
 #define FVA_TRACE 2u            /* record per-item start/end clock and CU id into `trace` */
+/* Persistent scheduler only: run every query block as an item of its own.
+ * Without it, two x-neighbouring query blocks (ix, ix + 1), ix even, of one
+ * (t, y) line that both hold at most 64 real tokens and are both unsplit run
+ * as one 128-row item over the union of their kept lists (each block on two
+ * of the four waves, each wave skipping the key blocks its block does not
+ * keep), so that every K/V tile either keeps is staged once. Each row still
+ * sees exactly its own key blocks in ascending order: the output is the
+ * same bit for bit. */
+#define FVA_SCHED_UNPAIRED 4u
 /* Persistent scheduler only: split every row keeping more than s blocks into
  * ceil(count / s) chunk items of at most s blocks (1 <= s <= 65535). Without
  * it the chunk size is automatic: max(32, ceil(total / 1024)) with total the
@@ -174,10 +183,12 @@ fva_status fva_route_sasa(const void* Q, const void* K, const fva_qkv_desc* desc
  * Workspace bytes needed by fva_attn for this shape and flags: the work
  * list and queue counters, room for counts and kv_idx (batch*heads*nb and
  * batch*heads*nb*nb int32) used when the caller passes them as NULL, one
- * 32-byte record per block, and the partial results of split rows: 66,560
+ * 32-byte record per block, the partial results of split rows: 66,560
  * bytes per chunk for at most 2048 chunks (automatic chunk size) or
- * batch*heads*nb*ceil(nb/s) chunks under FVA_SPLIT_BLOCKS(s); none under
- * FVA_SCHED_NAIVE.
+ * batch*heads*nb*ceil(nb/s) chunks under FVA_SPLIT_BLOCKS(s), none under
+ * FVA_SCHED_NAIVE; and the union lists of the query-block pairs,
+ * batch*heads*P*(nb + 1) int32 with P the pairs a head holds (none under
+ * FVA_SCHED_NAIVE or FVA_SCHED_UNPAIRED).
  */
 fva_status fva_attn_workspace_size(const fva_qkv_desc* desc, const fva_tiling* tiling, uint32_t flags,
                                    size_t* bytes);
@@ -202,14 +213,17 @@ int64_t fva_trace_words(const fva_qkv_desc* desc, const fva_tiling* tiling);
  *          workspace) or both given in the layout fva_route writes, and then
  *          they must describe block_mask exactly.
  * softmax_scale: <= 0 selects 1/sqrt(128).
- * flags: FVA_SCHED_PERSISTENT or FVA_SCHED_NAIVE, optionally | FVA_TRACE
- *        and | FVA_SPLIT_BLOCKS(s). A split row's chunks run as separate
- *        work items; their partial results (fp32) are merged in chunk order,
- *        so results stay deterministic.
+ * flags: FVA_SCHED_PERSISTENT or FVA_SCHED_NAIVE, optionally | FVA_TRACE,
+ *        | FVA_SCHED_UNPAIRED and | FVA_SPLIT_BLOCKS(s). A split row's chunks
+ *        run as separate work items; their partial results (fp32) are merged
+ *        in chunk order, so results stay deterministic. kv_idx rows are
+ *        taken in ascending order without repeats (as fva_route writes them):
+ *        a paired row is processed in that order whatever order it is given.
  * O: bf16, same strides as Q; every real token row is written.
  * trace: device int64 [fva_trace_words] when FVA_TRACE is set, else ignored.
  *        Row r = (b*heads + h)*nb + i gets {start, end, (xcc_id << 16) |
- *        hw_id low bits, shader-clock cycles} (unwritten for a split row),
+ *        hw_id low bits, shader-clock cycles} (unwritten for a split row;
+ *        the two rows of a pair share their item's time, half each),
  *        chunk c of a split row the same at batch*heads*nb + c (c < 2048);
  *        start and end are the 100 MHz constant device clock, the last word
  *        the item's elapsed engine-clock cycles (s_memtime), so that
@@ -342,8 +356,10 @@ fva_status fva_attn_fp8v(const void* Q, const void* K, const uint8_t* V8, const 
  *
  * Differences from fva_attn: counts and kv_idx are required (in the layout
  * fva_route writes; the mask itself is not read); flags may hold FVA_TRACE
- * only (FVA_SCHED_NAIVE and FVA_SPLIT_BLOCKS are rejected); no row is split
- * into chunks, so where fva_attn's automatic chunk size would split rows
+ * only (FVA_SCHED_NAIVE, FVA_SCHED_UNPAIRED and FVA_SPLIT_BLOCKS are
+ * rejected); every query block runs as its own item (no query-block pairs,
+ * whose union lists are not kept; pairing changes no output bit); no row is
+ * split into chunks, so where fva_attn's automatic chunk size would split rows
  * (few rows per workgroup slot) the output can differ from fva_attn's in the
  * last bits (the same sums in another order); everywhere else it is
  * identical. Inputs, O, trace and errors as for fva_attn.

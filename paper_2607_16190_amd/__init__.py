@@ -37,6 +37,7 @@ FVA_ERR_SCRATCH = -6
 FVA_SCHED_PERSISTENT = 0
 FVA_SCHED_NAIVE = 1
 FVA_TRACE = 2
+FVA_SCHED_UNPAIRED = 4
 
 FVA_TO_CURVE = 0
 FVA_FROM_CURVE = 1

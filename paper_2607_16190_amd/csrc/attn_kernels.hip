@@ -21,6 +21,14 @@
 // work on neighbouring query blocks (their kept K/V overlap in L2). A
 // workgroup whose queue is empty steals from the others. FVA_SCHED_NAIVE
 // launches the same item body once per item in head-major order.
+//
+// Query-block pairs: blocks of at most 64 real tokens (partial boxes at the
+// end of the t or y axis, or every block of a 64-token tiling) fill only two
+// of the four waves, and a CU's other workgroup cannot use the idle SIMDs
+// because its own waves move in step through their barriers. Two such
+// x-neighbours run as one item instead: each on two waves, over the union of
+// their kept lists (neighbouring blocks keep nearly the same key blocks), so
+// every SIMD works and each K/V tile is staged once for both.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -70,6 +78,15 @@ struct AttnParams {
   const BlockMap* bmap;  // [nb] block records
   const int4* chunks;    // [chunks] (row, first kept entry, end, 0) of split rows
   float* partials;       // [chunks][kPartialFloats] unnormalised O, reference, sum
+  // Query-block pairs (null: none). plist holds, per pair slot, the union of
+  // the two rows' kept lists in ascending block order, each entry
+  // j | (not kept by the first block) << 16 | (not kept by the second) << 17;
+  // pcount its length; psplit the chunk size of the plan (a pair is formed
+  // only when neither row is split).
+  const int32_t* plist;
+  const int32_t* pcount;
+  const int32_t* psplit;
+  int pairs_head;        // pair slots per head
   int64_t n_rows;        // batch * heads * nb
   int trace_chunks;      // chunk records the trace holds after the rows
   float c2;  // softmax scale * log2(e)
@@ -287,7 +304,11 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // One work item: query block `row` (= (b * heads + h) * nb + i) against the
 // kept-list entries [begin, end) of its row. partial == nullptr: the whole
 // row, normalised into O; otherwise one chunk of a split row, whose
-// unnormalised result goes to partial for the combine step.
+// unnormalised result goes to partial for the combine step. pslot >= 0: the
+// query-block pair (i, i + 1) of that slot, block i on waves 0-1 and block
+// i + 1 on waves 2-3, over the union of their kept lists; a wave skips the
+// key blocks its own block does not keep, so each row sees exactly its own
+// blocks in ascending order, as when the two run alone.
 //
 // F8 (the quantised-V variant): V comes as E4M3 tiles with per-channel
 // power-of-two scales; the probabilities of a whole block are rounded to
@@ -295,7 +316,7 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // tile), the scales entering as the MFMA's E8M0 block scales.
 template <bool F8>
 __device__ void process_item(const AttnParams& P, int row, int begin, int end, float* __restrict__ partial,
-                             unsigned char* __restrict__ Ks, unsigned char* __restrict__ Vs) {
+                             unsigned char* __restrict__ Ks, unsigned char* __restrict__ Vs, int pslot = -1) {
   const int nb = P.g.nb;
   const int bh = row / nb;
   const int i = row - bh * nb;
@@ -306,12 +327,15 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   const uint16_t* Kh = P.K + base;
   const uint16_t* Vh = P.V + base;
   uint16_t* Oh = P.O + base;
-  const BlockBox bi = block_box(P.g, i);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g4 = lane >> 4;
   const int l16 = lane & 15;
-  const int row0 = wave * 32;
+  const bool paired = pslot >= 0;
+  const int half = paired ? wave >> 1 : 0;  // which block of a pair
+  const int hbit = paired ? 1 << half : 0;  // this wave's skip bit in a pair's entries
+  const BlockBox bi = block_box(P.g, i + half);
+  const int row0 = paired ? 32 * (wave & 1) : 32 * wave;
   const bool active = row0 < bi.n;
 
   // FP8 variant: the head's E4M3 V tiles, and the E8M0 scale 127 + e_d of
@@ -333,12 +357,21 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   // counts and kv_idx are read through the scalar cache (constant address
   // space: the kernel never writes them). They come from the caller: clamp
   // so a bad list cannot address outside the tensors.
+  // A pair's list entries carry its skip bits from bit 16 on; kv_idx entries
+  // are block ids (< nb <= 1024), and only the bits below 16 are read as one.
   typedef __attribute__((address_space(4))) const int32_t const_i32;
-  const int full = min(max(((const const_i32*)P.counts)[row], 0), nb);
-  begin = min(max(begin, 0), full);
-  end = min(max(end, begin), full);
-  const const_i32* kvl = (const const_i32*)(P.kv_idx + (int64_t)row * nb + begin);
-  const int cnt = end - begin;
+  const const_i32* kvl;
+  int cnt;
+  if (paired) {
+    kvl = (const const_i32*)(P.plist + (int64_t)pslot * nb);
+    cnt = min(max(((const const_i32*)P.pcount)[pslot], 0), nb);
+  } else {
+    const int full = min(max(((const const_i32*)P.counts)[row], 0), nb);
+    begin = min(max(begin, 0), full);
+    end = min(max(end, begin), full);
+    kvl = (const const_i32*)(P.kv_idx + (int64_t)row * nb + begin);
+    cnt = end - begin;
+  }
 
   // Q_i^T as the B operand: lane holds query row l16 of each 16-row tile,
   // head dims 32ks + 8g4 .. +7.
@@ -394,9 +427,13 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   // block ahead (during the current block's softmax), so their scalar loads
   // never stall the copy of the next tiles.
   int roff[8];
-  const int jc = cnt > 0 ? min(max(kvl[0], 0), nb - 1) : 0;
+  const int e0 = cnt > 0 ? kvl[0] : 0;
+  const int e1 = cnt > 1 ? kvl[1] : 0;
+  const int jc = min(e0 & 0xFFFF, nb - 1);
   BlockMap mc = load_block_map(P.bmap, jc);
-  int j1 = cnt > 1 ? min(max(kvl[1], 0), nb - 1) : 0;
+  int j1 = min(e1 & 0xFFFF, nb - 1);
+  // skip bits of the current block (bits 0-1) and of the next (bits 2-3)
+  int fq = ((e0 >> 16) & 3) | (((e1 >> 16) & 3) << 2);
   if (cnt > 0) {
     row_offsets(P, mc, roff);
     if (wave < ngroups_of(mc.n)) {
@@ -704,23 +741,26 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
       // K_c landed (the four copies of V8_c, issued after it, may be in flight).
       wait_vmem<4>();
       tile_barrier();
+      const bool act = active && !(fq & hbit);
       i32x8 p8[2] = {i32x8{0, 0, 0, 0, 0, 0, 0, 0}, i32x8{0, 0, 0, 0, 0, 0, 0, 0}};
       int kb[2] = {0, 0};
       BlockMap mn;
       int j2 = 0;
       {
         f32x4 s[4][2];
-        if (active) s_phase(0, false, s);
-        // record of block c + 1 and the id of block c + 2 (clamped to the list)
+        if (act) s_phase(0, false, s);
+        // record of block c + 1 and the entry of block c + 2 (clamped to the list)
         mn = load_block_map(P.bmap, j1);
-        j2 = min(max(kvl[min(c + 2, cnt - 1)], 0), nb - 1);
-        if (active) softmax_f8(0, false, nj, s, p8, kb);
+        const int e2 = kvl[min(c + 2, cnt - 1)];
+        j2 = min(e2 & 0xFFFF, nb - 1);
+        fq = (fq >> 2) | (((e2 >> 16) & 3) << 2);
+        if (act) softmax_f8(0, false, nj, s, p8, kb);
       }
       {
         const bool run = ng > 2;
         const bool short_half = ng == 3;
         f32x4 s[4][2];
-        if (active && run) s_phase(1, short_half, s);
+        if (act && run) s_phase(1, short_half, s);
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the prefetched scalars
         wait_vmem<0>();                        // V8_c landed
         tile_barrier();                        // every wave is done with K_c and sees V8_c
@@ -731,9 +771,9 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
             issue_tile<false>(Kh, roff, Ks);
           }
         }
-        if (active && run) softmax_f8(1, short_half, nj, s, p8, kb);
+        if (act && run) softmax_f8(1, short_half, nj, s, p8, kb);
       }
-      if (active) {
+      if (act) {
         // B scale of the K block whose scale this lane supplies: lane groups
         // 0 and 1 scale the first half's keys, which carry the second half's
         // reference move
@@ -752,6 +792,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
     if (wave < ng) wait_vmem<8>(); else wait_vmem<0>();
     tile_barrier();
 
+    const bool act = active && !(fq & hbit);
     int ng_next = 0;
     BlockMap mn;
     int j2 = 0;
@@ -763,11 +804,13 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
       const bool short_half = hb == 1 && ng == 3;
       f32x4 s[4][2];
       bf16x8 pb[2][2];
-      if (active && run) s_phase(hb, short_half, s);
+      if (act && run) s_phase(hb, short_half, s);
       if (hb == 0) {
-        // record of block c + 1 and the id of block c + 2 (clamped to the list)
+        // record of block c + 1 and the entry of block c + 2 (clamped to the list)
         mn = load_block_map(P.bmap, j1);
-        j2 = min(max(kvl[min(c + 2, cnt - 1)], 0), nb - 1);
+        const int e2 = kvl[min(c + 2, cnt - 1)];
+        j2 = min(e2 & 0xFFFF, nb - 1);
+        fq = (fq >> 2) | (((e2 >> 16) & 3) << 2);
       }
       if (hb == 1) {
         tile_barrier();  // every wave is done with K_c
@@ -781,7 +824,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
           }
         }
       }
-      if (active && run) softmax_phase(hb, short_half, nj, s, pb);
+      if (act && run) softmax_phase(hb, short_half, nj, s, pb);
       if (hb == 0) {
         // The prefetched scalars have landed long ago; waiting for them here,
         // where no LDS read is in flight, keeps the PV fragment waits exact.
@@ -790,7 +833,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
         wait_vmem<0>();
         tile_barrier();
       }
-      if (active && run) pv_phase(hb, short_half, pb, s, negm);
+      if (act && run) pv_phase(hb, short_half, pb, s, negm);
     }
     tile_barrier();  // every wave is done with V_c
     if (c + 1 < cnt && wave < ng_next) issue_tile<true>(Vh, roff, Vs);
@@ -836,16 +879,28 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
 // Trace record r: rows first, then chunk items (chunk c at n_rows + c):
 // start and end on the 100 MHz constant clock, where the item ran, and the
 // shader-clock cycles (s_memtime) it took, so that the engine clock of the
-// run is the ratio of the two clocks.
-__device__ __forceinline__ void trace_item(const AttnParams& P, int64_t rec, int64_t t0, int64_t c0) {
-  if (P.trace && threadIdx.x == 0) {
-    const int64_t c1 = (int64_t)__builtin_amdgcn_s_memtime();
-    const int64_t t1 = (int64_t)wall_clock64();
-    int64_t* tr = P.trace + rec * 4;
+// run is the ratio of the two clocks. A pair's item fills the records of
+// both its rows, splitting its time evenly between them. One thread writes.
+__device__ __forceinline__ void trace_record(const AttnParams& P, int64_t rec, bool pair, int64_t t0, int64_t t1,
+                                             int64_t cycles) {
+  const int64_t loc = (int64_t)hw_location();
+  int64_t* tr = P.trace + rec * 4;
+  if (pair) {
+    const int64_t tm = t0 + (t1 - t0) / 2;
+    const int64_t cm = cycles / 2;
+    tr[0] = t0;
+    tr[1] = tm;
+    tr[2] = loc;
+    tr[3] = cm;
+    tr[4] = tm;
+    tr[5] = t1;
+    tr[6] = loc;
+    tr[7] = cycles - cm;
+  } else {
     tr[0] = t0;
     tr[1] = t1;
-    tr[2] = (int64_t)hw_location();
-    tr[3] = c1 - c0;
+    tr[2] = loc;
+    tr[3] = cycles;
   }
 }
 
@@ -858,7 +913,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams 
   process_item<F8>(P, blockIdx.x, 0, P.g.nb, nullptr, ks_tile, vs_tile);
   if (P.trace) {
     __syncthreads();
-    trace_item(P, blockIdx.x, t0, c0);
+    if (threadIdx.x == 0) {
+      const int64_t c1 = (int64_t)__builtin_amdgcn_s_memtime();
+      trace_record(P, blockIdx.x, false, t0, (int64_t)wall_clock64(), c1 - c0);
+    }
   }
 }
 
@@ -866,6 +924,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams 
 // workgroups pull from the queue of the XCD they run on and steal from the
 // others once theirs is empty.
 constexpr int kQueues = 8;
+
+// Role of row r (= bh * nb + i) under query-block pairing with chunk size S:
+// 1 when it starts a pair (its item runs rows r and r + 1), 2 when it is the
+// second row of a pair (its item does nothing), 0 otherwise. A pair is formed
+// only when neither row is split (kept count <= S). The plan, the pair-list
+// kernel and the persistent kernel all decide it with this function.
+__device__ __forceinline__ int pair_role(const Geometry& g, const int32_t* __restrict__ counts, int r, int S) {
+  const int i = r % g.nb;
+  auto whole = [&](int rr) { return min(max(counts[rr], 0), g.nb) <= S; };
+  if (pair_slot(g, i) >= 0) return (whole(r) && whole(r + 1)) ? 1 : 0;
+  if (i > 0 && pair_slot(g, i - 1) >= 0) return (whole(r - 1) && whole(r)) ? 2 : 0;
+  return 0;
+}
 
 __device__ __forceinline__ int xcc_id() {
   uint32_t xcc;
@@ -881,8 +952,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
   __shared__ __align__(16) unsigned char vs_tile[F8 ? kV8TileBytes : kTileBytes];
   __shared__ int next_slot, next_q;
   int q = xcc_id() % kQueues;
+  // The trace record of an item is written at the top of the next iteration,
+  // by thread 0 together with the queue pop: the loop then holds a single
+  // region that only thread 0 runs, so the compiler keeps every lane of
+  // every wave on one path through the loop and its barriers.
+  int64_t prec = -1, pt0 = 0, pt1 = 0, pcyc = 0;
+  bool ppair = false;
   for (;;) {
     if (threadIdx.x == 0) {
+      if (prec >= 0) trace_record(P, prec, ppair, pt0, pt1, pcyc);
       int slot = -1, qq = q;
       for (int t = 0; t < kQueues; ++t) {
         qq = (q + t) % kQueues;
@@ -905,19 +983,37 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
     const int item = __builtin_amdgcn_readfirstlane(items[slot]);
     const int64_t t0 = (int64_t)wall_clock64();
     const int64_t c0 = P.trace ? (int64_t)__builtin_amdgcn_s_memtime() : 0;
-    int64_t rec;
+    // One call site for every kind of item (rows, pairs, chunks), so that the
+    // item body is inlined once.
+    int row = item, begin = 0, end = P.g.nb, pslot = -1;
+    float* partial = nullptr;
+    int64_t rec = item;
     if (item >= 0) {
-      process_item<F8>(P, item, 0, P.g.nb, nullptr, ks_tile, vs_tile);
-      rec = item;
+      const int role = P.plist ? pair_role(P.g, P.counts, item, *P.psplit) : 0;
+      if (role == 1) {
+        const int bh = item / P.g.nb;
+        pslot = bh * P.pairs_head + pair_slot(P.g, item - bh * P.g.nb);
+      }
+      rec = role == 2 ? -1 : item;  // the pair's item records the second row
     } else {
       const int c = -1 - item;
       typedef __attribute__((address_space(4))) const int32_t const_i32;
       const const_i32* ch = (const const_i32*)(P.chunks + c);
-      process_item<F8>(P, ch[0], ch[1], ch[2], P.partials + (int64_t)c * kPartialFloats, ks_tile, vs_tile);
-      rec = c < P.trace_chunks ? P.n_rows + c : -1;
+      row = ch[0];
+      begin = ch[1];
+      end = ch[2];
+      partial = P.partials + (int64_t)c * kPartialFloats;
+      rec = c < P.trace_chunks ? P.n_rows + c : -2;
     }
+    if (rec != -1) process_item<F8>(P, row, begin, end, partial, ks_tile, vs_tile, pslot);
     __syncthreads();  // the next item's copies overwrite the tiles; next_slot is rewritten
-    if (P.trace && rec >= 0) trace_item(P, rec, t0, c0);
+    if (P.trace) {
+      prec = rec;
+      ppair = pslot >= 0;
+      pt0 = t0;
+      pt1 = (int64_t)wall_clock64();
+      pcyc = (int64_t)__builtin_amdgcn_s_memtime() - c0;
+    }
   }
 }
 
@@ -936,6 +1032,10 @@ constexpr int kPlanLdsHeads = 1024;  // heads whose queue bookkeeping the plan k
 // (the sum of ceil(c / S) over rows with c > S is at most 2 * total / S). If
 // the chunks would exceed chunk_cap, no row is split.
 //
+// Pairs (pairing != 0): the final S goes to *psplit for the pair-list and
+// attention kernels; a pair's first row costs its larger kept count + 1 (the
+// union it runs is about that long) and its second row 1 (an empty item).
+//
 // Queues: heads are taken in decreasing order of cost. Each head's query
 // blocks are cut into kQueues contiguous runs of about equal cost, run x going
 // to queue x (the items of a split row stay together), so all XCDs work on the
@@ -950,7 +1050,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
                                                    int32_t* __restrict__ qbase, int32_t* __restrict__ qctr,
                                                    int32_t* __restrict__ hscratch, int32_t* __restrict__ rscratch,
                                                    int4* __restrict__ chunks, int4* __restrict__ splits,
-                                                   int32_t* __restrict__ n_split) {
+                                                   int32_t* __restrict__ n_split, int pairing,
+                                                   int32_t* __restrict__ psplit) {
   __shared__ long long wtot[16];
   __shared__ int lds_order[kPlanLdsHeads];
   __shared__ int lds_len[kPlanLdsHeads * kQueues];
@@ -969,7 +1070,6 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
     const int c = counts[r];
     return c < 0 ? 0 : (c > nb ? nb : c);
   };
-  auto cost_of = [&](int h, int r) { return kept_of(h * nb + r) + 1; };
 
   // 0. chunk size
   long long tsum = 0;
@@ -1034,6 +1134,13 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   __syncthreads();
   // items before row r (ipre[r])
   auto ipre = [&](int r) { return may_split ? r + cpre[r] - spre[r] : r; };
+  if (pairing && threadIdx.x == 0) *psplit = S;
+  auto cost_of = [&](int h, int i) {
+    const int r = h * nb + i;
+    const int role = pairing ? pair_role(g, counts, r, S) : 0;
+    if (role == 1) return max(kept_of(r), kept_of(r + 1)) + 1;
+    return role == 2 ? 1 : kept_of(r) + 1;
+  };
 
   // 2. head costs and equal-cost runs (one wave per head)
   for (int h = wave; h < n_heads; h += nwaves) {
@@ -1158,6 +1265,54 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   if (threadIdx.x < kQueues) qctr[threadIdx.x] = 0;
 }
 
+// Union lists of the query-block pairs, one wave per row (rows that do not
+// start a pair leave at once): the two rows' kept sets become bitmaps in LDS,
+// read back in ascending block order as entries j | (j not kept by the first
+// row) << 16 | (j not kept by the second row) << 17. An entry repeated in a
+// kept list counts once.
+constexpr int kPairWords = kMaxBlocks / 64;
+
+__global__ __launch_bounds__(256) void pair_list_kernel(const int32_t* __restrict__ counts,
+                                                        const int32_t* __restrict__ kv_idx, int rows, Geometry g,
+                                                        int pairs_head, const int32_t* __restrict__ psplit,
+                                                        int32_t* __restrict__ plist, int32_t* __restrict__ pcount) {
+  __shared__ unsigned long long bits[4][2 * kPairWords];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nb = g.nb;
+  const int S = *psplit;
+  unsigned long long* bw = bits[wave];
+  for (int r = blockIdx.x * 4 + wave; r < rows; r += gridDim.x * 4) {
+    if (pair_role(g, counts, r, S) != 1) continue;
+    const int bh = r / nb;
+    const int slot = bh * pairs_head + pair_slot(g, r - bh * nb);
+    if (lane < 2 * kPairWords) bw[lane] = 0ull;
+    wave_sync();
+    for (int s = 0; s < 2; ++s) {
+      const int c = min(max(counts[r + s], 0), nb);
+      const int32_t* kv = kv_idx + (int64_t)(r + s) * nb;
+      for (int a = lane; a < c; a += 64) {
+        const int j = min(max(kv[a], 0), nb - 1);
+        atomicOr(&bw[s * kPairWords + (j >> 6)], 1ull << (j & 63));
+      }
+    }
+    wave_sync();
+    int32_t* out = plist + (int64_t)slot * nb;
+    int n = 0;
+    for (int w = 0; w * 64 < nb; ++w) {
+      const int j = 64 * w + lane;
+      const int ka = (int)((bw[w] >> lane) & 1ull);
+      const int kb = (int)((bw[kPairWords + w] >> lane) & 1ull);
+      const bool keep = (ka | kb) != 0;  // bits past nb are never set
+      const uint64_t m = __ballot(keep);
+      if (keep) out[n + lanes_below(m)] = j | ((ka ^ 1) << 16) | ((kb ^ 1) << 17);
+      n += __popcll(m);
+    }
+    if (lane == 0) pcount[slot] = n;
+    wave_sync();  // the bitmaps are cleared for the next row only after every lane read them
+  }
+}
+
 // Merges the chunks of every split row (one workgroup per row at a time, in
 // chunk order, so the result is deterministic): with m_c the chunk's
 // exponent reference, l_c its sum of P and O_c its unnormalised output,
@@ -1276,6 +1431,10 @@ struct AttnWorkspace {
   int4* splits;      // [cap]
   float* partials;   // [cap][kPartialFloats]
   BlockMap* bmap;    // [nb]
+  int32_t* plist;    // [pairs][nb]   union lists of query-block pairs (null: no pairing)
+  int32_t* pcount;   // [pairs]
+  int32_t* psplit;   // [1]           the plan's chunk size
+  int pairs_head;    // pairs per head
   int cap;           // chunk records
   size_t bytes;
 };
@@ -1293,10 +1452,17 @@ int chunk_cap(int batch, int heads, int nb, uint32_t flags) {
   return (int)std::min<int64_t>(cap, (int64_t)1 << 28);
 }
 
+// Query-block pairs per head under these flags: none for the naive grid,
+// under FVA_SCHED_UNPAIRED and in the allocation-free call.
+int pairs_of(const Geometry& g, uint32_t flags, bool lean) {
+  return (lean || (flags & 5u)) ? 0 : pairs_per_head(g);
+}
+
 // lean: the layout of the allocation-free call -- no room for rebuilt counts
-// and kept lists (the caller passes them) and no chunk items (no row is
-// split, so no partial results are kept).
-AttnWorkspace carve(void* base, int batch, int heads, int nb, uint32_t flags, bool lean = false) {
+// and kept lists (the caller passes them), no chunk items (no row is split,
+// so no partial results are kept) and no query-block pairs.
+AttnWorkspace carve(void* base, int batch, int heads, const Geometry& g, uint32_t flags, bool lean = false) {
+  const int nb = g.nb;
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t rows = (size_t)batch * heads * nb;
   const size_t nh = (size_t)batch * heads;
@@ -1329,13 +1495,24 @@ AttnWorkspace carve(void* base, int batch, int heads, int nb, uint32_t flags, bo
   off += al(cap * kPartialFloats * sizeof(float));
   w.bmap = reinterpret_cast<BlockMap*>(p + off);
   off += al((size_t)nb * sizeof(BlockMap));
+  w.pairs_head = pairs_of(g, flags, lean);
+  const size_t pairs = nh * (size_t)w.pairs_head;
+  w.plist = w.pcount = w.psplit = nullptr;
+  if (pairs > 0) {
+    w.plist = reinterpret_cast<int32_t*>(p + off);
+    off += al(pairs * nb * 4);
+    w.pcount = reinterpret_cast<int32_t*>(p + off);
+    off += al(pairs * 4);
+    w.psplit = reinterpret_cast<int32_t*>(p + off);
+    off += al(4);
+  }
   w.bytes = off;
   return w;
 }
 }  // namespace
 
-size_t attn_workspace_bytes(int batch, int heads, int nb, uint32_t flags) {
-  return carve(nullptr, batch, heads, nb, flags).bytes;
+size_t attn_workspace_bytes(int batch, int heads, const Geometry& g, uint32_t flags) {
+  return carve(nullptr, batch, heads, g, flags).bytes;
 }
 
 // ---- Allocation-free attention ---------------------------------------------
@@ -1347,8 +1524,8 @@ size_t attn_workspace_bytes(int batch, int heads, int nb, uint32_t flags) {
 constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
 static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 
-size_t attn_noalloc_bytes(int batch, int heads, int nb) {
-  return carve(nullptr, batch, heads, nb, 0u, true).bytes;
+size_t attn_noalloc_bytes(int batch, int heads, const Geometry& g) {
+  return carve(nullptr, batch, heads, g, 0u, true).bytes;
 }
 
 size_t attn_noalloc_capacity() { return kNoAllocScratchBytes; }
@@ -1383,7 +1560,7 @@ hipError_t launch_attn(const AttnArgs& a) {
   const Geometry g = make_geometry(a.T, a.H, a.W, a.bt, a.bh, a.bw);
   const int n_items = a.batch * a.heads * g.nb;
   if (n_items == 0) return hipSuccess;
-  const AttnWorkspace ws = carve(a.workspace, a.batch, a.heads, g.nb, a.flags, a.lean);
+  const AttnWorkspace ws = carve(a.workspace, a.batch, a.heads, g, a.flags, a.lean);
   int32_t* ws_counts = ws.counts;
   int32_t* ws_kv = ws.kv;
   DeviceInfo info;
@@ -1423,6 +1600,10 @@ hipError_t launch_attn(const AttnArgs& a) {
   P.trace_chunks = 4 * kSplitSlots;
   P.c2 = a.scale * 1.4426950408889634f;
   P.trace = (a.flags & 2u) ? a.trace : nullptr;
+  P.plist = ws.plist;
+  P.pcount = ws.pcount;
+  P.psplit = ws.psplit;
+  P.pairs_head = ws.pairs_head;
 
   hipLaunchKernelGGL(block_table_kernel, dim3((g.nb + 255) / 256), dim3(256), 0, a.stream, g, ws.bmap);
   e = hipGetLastError();
@@ -1437,9 +1618,17 @@ hipError_t launch_attn(const AttnArgs& a) {
   }
   const int forced = (int)((a.flags >> 8) & 0xFFFFu);
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, a.batch * a.heads, g, kSplitSlots, forced,
-                     ws.cap, ws.items, ws.qbase, ws.qctr, ws.hscratch, ws.rscratch, ws.chunks, ws.splits, ws.n_split);
+                     ws.cap, ws.items, ws.qbase, ws.qctr, ws.hscratch, ws.rscratch, ws.chunks, ws.splits, ws.n_split,
+                     ws.plist ? 1 : 0, ws.psplit);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (ws.plist) {
+    const int pgrid = std::max(1, std::min((n_items + 3) / 4, 4 * info.cus));
+    hipLaunchKernelGGL(pair_list_kernel, dim3(pgrid), dim3(256), 0, a.stream, counts, kv_idx, n_items, g,
+                       ws.pairs_head, ws.psplit, ws.plist, ws.pcount);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   int grid = info.cus * (f8 ? info.per_cu8 : info.per_cu);
   if ((int64_t)grid > (int64_t)n_items + ws.cap) grid = n_items + ws.cap;
   if (f8)

@@ -48,7 +48,7 @@ fva_status check_curve_grid(int32_t T, int32_t H, int32_t W) {
 }
 
 // Scheduling bits, the trace bit and a forced chunk size in bits 8..23.
-constexpr uint32_t kAttnFlags = 3u | (0xFFFFu << 8);
+constexpr uint32_t kAttnFlags = 7u | (0xFFFFu << 8);
 
 // Attention indexes its work items -- batch * heads * nb query blocks plus
 // the chunk items of split rows (at most 2048 with the automatic chunk size,
@@ -86,7 +86,8 @@ fva_status fva_attn_workspace_size(const fva_qkv_desc* desc, const fva_tiling* t
   const fva_status s = check_shape(desc, tiling, &nb);
   if (s != FVA_OK) return s;
   if (!attn_items_fit(desc, nb, flags)) return FVA_ERR_UNSUPPORTED;
-  *bytes = fva::attn_workspace_bytes(desc->batch, desc->heads, nb, flags);
+  const fva::Geometry g = fva::make_geometry(tiling->T, tiling->H, tiling->W, tiling->bt, tiling->bh, tiling->bw);
+  *bytes = fva::attn_workspace_bytes(desc->batch, desc->heads, g, flags);
   return FVA_OK;
 }
 
@@ -201,7 +202,8 @@ fva_status attn_common(const void* Q, const void* K, const void* V, const uint8_
   if (!aligned16(Q) || !aligned16(K) || !aligned16(O)) return FVA_ERR_INVALID_ARG;
   if (V && !aligned16(V)) return FVA_ERR_INVALID_ARG;
   if (V8 && !aligned16(V8)) return FVA_ERR_INVALID_ARG;
-  const size_t need = fva::attn_workspace_bytes(desc->batch, desc->heads, nb, flags);
+  const fva::Geometry g = fva::make_geometry(tiling->T, tiling->H, tiling->W, tiling->bt, tiling->bh, tiling->bw);
+  const size_t need = fva::attn_workspace_bytes(desc->batch, desc->heads, g, flags);
   if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return FVA_ERR_WORKSPACE;
   fva::AttnArgs a;
   a.Q = Q;
@@ -257,7 +259,8 @@ fva_status fva_attn_noalloc(const void* Q, const void* K, const void* V, const f
   if (s != FVA_OK) return s;
   if (!attn_items_fit(desc, nb, 1u)) return FVA_ERR_UNSUPPORTED;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return FVA_ERR_INVALID_ARG;
-  if (fva::attn_noalloc_bytes(desc->batch, desc->heads, nb) > fva::attn_noalloc_capacity()) return FVA_ERR_SCRATCH;
+  const fva::Geometry g = fva::make_geometry(tiling->T, tiling->H, tiling->W, tiling->bt, tiling->bh, tiling->bw);
+  if (fva::attn_noalloc_bytes(desc->batch, desc->heads, g) > fva::attn_noalloc_capacity()) return FVA_ERR_SCRATCH;
   fva::AttnArgs a;
   a.Q = Q;
   a.K = K;

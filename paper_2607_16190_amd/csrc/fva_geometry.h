@@ -53,6 +53,42 @@ __host__ __device__ inline BlockBox block_box(const Geometry& g, int i) {
   return b;
 }
 
+// Query-block pairs. Two x-neighbouring blocks (ix, ix + 1), ix even, of the
+// same (t, y) line are one pair when both hold at most 64 real tokens; the
+// attention then runs them as one 128-row work item (each block on two
+// waves) that stages every key block kept by either once. Block ix is not the
+// last of its line, so its x extent is bw and block ix + 1 is no larger: a
+// line pairs all its floor(nbx / 2) pairs or none, decided by et * ey * bw.
+__host__ __device__ inline bool line_pairs(const Geometry& g, int et, int ey) { return et * ey * g.bw <= 64; }
+
+// Lines of t-row it (extent et) that pair.
+__host__ __device__ inline int paired_lines_of_row(const Geometry& g, int et) {
+  const int ey_last = g.H - (g.nby - 1) * g.bh;
+  return (g.nby - 1) * (line_pairs(g, et, g.bh) ? 1 : 0) + (line_pairs(g, et, ey_last) ? 1 : 0);
+}
+
+// Pairs in one head (every head has the same).
+__host__ __device__ inline int pairs_per_head(const Geometry& g) {
+  const int et_last = g.T - (g.nbt - 1) * g.bt;
+  const int lines = (g.nbt - 1) * paired_lines_of_row(g, g.bt) + paired_lines_of_row(g, et_last);
+  return lines * (g.nbx / 2);
+}
+
+// Slot of the pair whose first block is i within its head (pairs numbered in
+// raster order of their first block), or -1 when i does not start a pair.
+__host__ __device__ inline int pair_slot(const Geometry& g, int i) {
+  const int it = i / (g.nby * g.nbx);
+  const int rem = i - it * (g.nby * g.nbx);
+  const int iy = rem / g.nbx;
+  const int ix = rem - iy * g.nbx;
+  const int et = min(g.bt, g.T - it * g.bt);
+  const int ey = min(g.bh, g.H - iy * g.bh);
+  if ((ix & 1) || ix + 1 >= g.nbx || !line_pairs(g, et, ey)) return -1;
+  // t-rows before it are full in t, lines before iy in this row full in y
+  const int lines_before = it * paired_lines_of_row(g, g.bt) + iy * (line_pairs(g, et, g.bh) ? 1 : 0);
+  return lines_before * (g.nbx / 2) + ix / 2;
+}
+
 // Global token index of the r-th real token (local raster order) of a box.
 __host__ __device__ inline int box_token(const Geometry& g, const BlockBox& b, int r) {
   const int plane = b.ey * b.ex;

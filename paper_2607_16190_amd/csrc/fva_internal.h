@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "fva_geometry.h"
+
 namespace fva {
 
 struct RouteArgs {
@@ -63,7 +65,7 @@ struct QuantizeArgs {
 
 size_t route_workspace_bytes(int batch, int heads, int nb);
 size_t route_sasa_workspace_bytes(int batch, int heads, int nb);
-size_t attn_workspace_bytes(int batch, int heads, int nb, uint32_t flags);
+size_t attn_workspace_bytes(int batch, int heads, const Geometry& g, uint32_t flags);
 int64_t attn_trace_words(int batch, int heads, int nb);
 
 hipError_t launch_route(const RouteArgs& a);
@@ -72,7 +74,7 @@ hipError_t launch_attn(const AttnArgs& a);
 // Allocation-free attention: scratch bytes a shape needs, the capacity of
 // the library's static device scratch, and the launch (persistent scheduler,
 // caller's counts and kept lists, no split rows) on that scratch.
-size_t attn_noalloc_bytes(int batch, int heads, int nb);
+size_t attn_noalloc_bytes(int batch, int heads, const Geometry& g);
 size_t attn_noalloc_capacity();
 hipError_t launch_attn_noalloc(const AttnArgs& a);
 

@@ -60,18 +60,64 @@ def test_workspace_sizes():
     heads = 40
     part = 66560  # one chunk's partial result: 128 x 128 fp32 O, 128 references, 128 sums
 
-    def attn_ws(cap):
+    def attn_ws(cap, pairs=0):
         # counts, kept lists, queue items (rows + chunks), 9 queue bases, 8 queue
         # counters, per-head plan scratch, per-row prefixes, split count, chunk and
-        # split records, partial results, one 32-byte record per block
-        return (al(rows * 4) + al(rows * nb * 4) + al((rows + cap) * 4) + al(9 * 4) + al(8 * 4)
-                + al(heads * 19 * 4) + al(2 * (rows + 1) * 4) + al(4) + 2 * al(cap * 16) + al(cap * part)
-                + al(nb * 32))
+        # split records, partial results, one 32-byte record per block, then the
+        # query-block pairs' union lists, their lengths and the plan's chunk size
+        ws = (al(rows * 4) + al(rows * nb * 4) + al((rows + cap) * 4) + al(9 * 4) + al(8 * 4)
+              + al(heads * 19 * 4) + al(2 * (rows + 1) * 4) + al(4) + 2 * al(cap * 16) + al(cap * part)
+              + al(nb * 32))
+        if pairs:
+            ws += al(pairs * nb * 4) + al(pairs * 4) + al(4)
+        return ws
 
-    assert fva.fva_attn_workspace_size(desc(), T720) == attn_ws(2048)
+    # 720p: the 60 blocks of the last (one-frame) t-row hold 64 or 40 tokens,
+    # 6 lines of 10 blocks, so 5 x-pairs per line and 30 per head
+    pairs = heads * 30
+    assert fva.fva_attn_workspace_size(desc(), T720) == attn_ws(2048, pairs)
+    assert fva.fva_attn_workspace_size(desc(), T720, fva.FVA_SCHED_UNPAIRED) == attn_ws(2048)
     assert fva.fva_attn_workspace_size(desc(), T720, fva.FVA_SCHED_NAIVE) == attn_ws(0)
-    assert fva.fva_attn_workspace_size(desc(), T720, fva.FVA_SPLIT_BLOCKS(200)) == attn_ws(rows * 4)
+    assert fva.fva_attn_workspace_size(desc(), T720, fva.FVA_SPLIT_BLOCKS(200)) == attn_ws(rows * 4, pairs)
     assert fva.fva_trace_words(desc(), T720) == (rows + 2048) * 4
+
+
+def _pairs_by_definition(T, H, W, bt, bh, bw):
+    """Query-block pairs of one head, counted block by block: x-neighbours
+    (ix, ix + 1) with ix even of one (t, y) line, both holding <= 64 tokens."""
+    from oracle import tile_geometry
+
+    geo = tile_geometry(T, H, W, bt, bh, bw)
+    n = geo.block_sizes.reshape(geo.nbt, geo.nby, geo.nbx)
+    return int(((n[:, :, 0:geo.nbx - 1:2] <= 64) & (n[:, :, 1::2] <= 64)).sum())
+
+
+@pytest.mark.parametrize(
+    "grid,tile,expect",
+    [
+        ((21, 45, 80), (2, 8, 8), 30),      # 720p: the one-frame last t-row
+        ((31, 45, 80), (2, 8, 8), 30),      # long clip
+        ((21, 30, 52), (2, 8, 8), None),    # 480p: partial boxes on all three axes
+        ((3, 16, 16), (1, 8, 8), 6),        # 64-token boxes: every line pairs
+        ((5, 17, 23), (1, 8, 8), None),     # odd block counts per line
+        ((9, 20, 40), (2, 4, 8), None),     # 64-token boxes of another shape
+        ((1, 1, 60000), (1, 1, 64), 469),   # curve blocks of 64 tokens (the last holds 32)
+        ((1, 1, 75600), (1, 1, 128), 0),    # curve blocks of 128: none
+    ],
+)
+def test_pair_count_matches_definition(grid, tile, expect):
+    T, H, W = grid
+    want = _pairs_by_definition(T, H, W, *tile)
+    if expect is not None:
+        assert want == expect
+    heads = 3
+    d = fva._Desc(1, heads, T * H * W, 128, heads * T * H * W * 128, T * H * W * 128, 128)
+    t = fva.Tiling(T, H, W, *tile)
+    nb = fva.fva_num_blocks(t)
+    al = lambda x: (x + 255) // 256 * 256
+    extra = fva.fva_attn_workspace_size(d, t) - fva.fva_attn_workspace_size(d, t, fva.FVA_SCHED_UNPAIRED)
+    P = heads * want
+    assert extra == ((al(P * nb * 4) + al(P * 4) + al(4)) if P else 0)
 
 
 @pytest.mark.parametrize(
@@ -301,6 +347,7 @@ def test_noalloc_scratch_limit_and_argument_errors():
     assert "static" in fva.fva_status_string(fva.FVA_ERR_SCRATCH)
     assert _noalloc(flags=fva.FVA_SCHED_NAIVE) == fva.FVA_ERR_INVALID_ARG
     assert _noalloc(flags=fva.FVA_SPLIT_BLOCKS(4)) == fva.FVA_ERR_INVALID_ARG
+    assert _noalloc(flags=fva.FVA_SCHED_UNPAIRED) == fva.FVA_ERR_INVALID_ARG
     assert _noalloc(flags=fva.FVA_TRACE, trace=None) == fva.FVA_ERR_INVALID_ARG
     assert _noalloc(counts=None) == fva.FVA_ERR_INVALID_ARG
     assert _noalloc(kv=None) == fva.FVA_ERR_INVALID_ARG
