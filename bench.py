@@ -82,14 +82,40 @@ def source_digest(*paths):
     return h.hexdigest()[:16]
 
 
-def imbalance(trace, counts):
+def plan_costs(counts, tiling, paired):
+    """Per-row cost the persistent plan balances: kept blocks + 1, except that
+    a query-block pair (x-neighbours ix even / ix + 1 of one (t, y) line, both
+    with at most 64 tokens, neither split) costs its larger row + 1 on its
+    first row and 1 on its second (the library's pairing rule, restated)."""
+    c = np.clip(counts.reshape(-1, counts.shape[-1]).astype(np.int64), 0, counts.shape[-1])
+    cost = c + 1
+    if not paired:
+        return cost.reshape(-1)
+    nbx = -(-tiling.W // tiling.bw)
+    n = block_sizes((tiling.T, tiling.H, tiling.W), (tiling.bt, tiling.bh, tiling.bw)).reshape(-1, nbx)
+    n = n.reshape(-1, -(-tiling.H // tiling.bh), nbx)
+    first = np.zeros(n.shape, bool)
+    first[:, :, 0:nbx - 1:2] = (n[:, :, 0:nbx - 1:2] <= 64) & (n[:, :, 1::2] <= 64)
+    first = np.nonzero(first.reshape(-1))[0]
+    S = max(32, -(-int((c + 1).sum()) // 1024))  # the automatic chunk size
+    a, b = c[:, first], c[:, first + 1]
+    formed = (a <= S) & (b <= S)
+    cost[:, first] = np.where(formed, np.maximum(a, b) + 1, cost[:, first])
+    cost[:, first + 1] = np.where(formed, 1, cost[:, first + 1])
+    return cost.reshape(-1)
+
+
+def imbalance(trace, counts, tiling=None, paired=False):
     """Per-CU and per-XCD load figures from an FVA_TRACE record.
 
     Records: one per (b, h, i) row, then one per chunk item of a split row
-    (a split row's own record stays empty). CU = (xcc, bits 8.. of HW_ID);
-    busy = sum of item durations on the CU. rho = max/mean over XCDs of summed
-    item time, and of summed kept blocks over the unsplit rows (Eq. 2 with
-    XCDs as ranks).
+    (a split row's own record stays empty; the two rows of a query-block
+    pair share their item's time). CU = (xcc, bits 8.. of HW_ID); busy =
+    sum of item durations on the CU. rho = max/mean over XCDs of summed item
+    time, of summed kept blocks over the unsplit rows (Eq. 2 with XCDs as
+    ranks), and of summed plan cost (kept blocks + 1, a pair costing about
+    one row: with pairs the plan balances cost, so kept blocks per XCD
+    differ by design).
     """
     tr = trace.reshape(-1, 4)
     rows = counts.size
@@ -102,8 +128,13 @@ def imbalance(trace, counts):
     busy = np.bincount(inv, weights=dur)
     xb = np.bincount(xcc, weights=dur, minlength=8)
     row_used = used[:rows]
-    xc = np.bincount(tr[:rows, 2][row_used] >> 16, weights=counts.reshape(-1)[row_used].astype(np.float64),
-                     minlength=8)
+    row_xcc = tr[:rows, 2][row_used] >> 16
+    xc = np.bincount(row_xcc, weights=counts.reshape(-1)[row_used].astype(np.float64), minlength=8)
+    res = {}
+    if tiling is not None:
+        cost = plan_costs(counts, tiling, paired)
+        xk = np.bincount(row_xcc, weights=cost[row_used].astype(np.float64), minlength=8)
+        res["xcd_cost_rho"] = round(float(xk.max() / xk.mean()), 4)
     span = float(tr[used, 1].max() - tr[used, 0].min()) / 100.0  # 100 MHz clock -> us
     # engine clock: shader cycles (word 3) over the 100 MHz constant clock
     sclk = float(tr[used, 3].sum()) * 100.0 / float((tr[used, 1] - tr[used, 0]).sum())
@@ -113,6 +144,7 @@ def imbalance(trace, counts):
         "cu_busy_max_over_mean": round(float(busy.max() / busy.mean()), 4),
         "xcd_time_rho": round(float(xb.max() / xb.mean()), 4),
         "xcd_blocks_rho": round(float(xc.max() / xc.mean()), 4),
+        **res,
         "chunk_items": int(used[rows:].sum()),
         "span_us": round(span, 1),
     }
@@ -177,23 +209,23 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "f5708f4d3f7424be",
+    "source_digest": "c61ab54109991c05",
     "bytes": {
-        "720p": ((107809152 + 107751492) // 2 * 2 + 759685) * 1024,
-        "720p-hilbert": ((80433327 + 80481098) // 2 * 2 + 759862) * 1024,
-        "720p-fp8v": ((69018673 + 69564284) // 2 * 2 + 758044) * 1024,
-        "720p-hilbert-fp8v": ((67994091 + 67917736) // 2 * 2 + 757982) * 1024,
+        "720p": ((111079208 + 112869768) // 2 * 2 + 758161) * 1024,
+        "720p-hilbert": ((77530191 + 78035132) // 2 * 2 + 758323) * 1024,
+        "720p-fp8v": ((70731104 + 70544653) // 2 * 2 + 758578) * 1024,
+        "720p-hilbert-fp8v": ((66796168 + 66587147) // 2 * 2 + 758506) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "cd3c88b9dc4dee67",
+    "source_digest": "892b2b78073cf628",
     "bytes": {
-        "720p": ((756174 + 29278 + 71517) * 2 + 53760 + 142451 + 49285) * 1024,
-        "720p-hilbert": ((756151 + 25318 + 58247) * 2 + 47360 + 117177 + 39989) * 1024,
-        "720p-fp8v": ((756173 + 29322 + 71553) * 2 + 53760 + 142328 + 49285) * 1024,
-        "720p-hilbert-fp8v": ((756149 + 25310 + 58231) * 2 + 47360 + 117559 + 39989) * 1024,
+        "720p": ((756174 + 29199 + 71521) * 2 + 53760 + 142494 + 49285) * 1024,
+        "720p-hilbert": ((756151 + 25338 + 58266) * 2 + 47360 + 117253 + 39989) * 1024,
+        "720p-fp8v": ((756174 + 29254 + 71556) * 2 + 53760 + 142399 + 49292) * 1024,
+        "720p-hilbert-fp8v": ((756150 + 25385 + 58256) * 2 + 47360 + 117109 + 39989) * 1024,
     },
 }
 
@@ -287,7 +319,8 @@ def extra_workloads(torch, fva, synth, dev, reps=3):
         fva.fva_attn(q, k, v, tiling, b["mask"], b["counts"], b["kv"], flags=fl | fva.FVA_TRACE, out=b["out"],
                      workspace=b["ws_a"], trace=trace)
         torch.cuda.synchronize()
-        res[name] = {"attn_ms": round(t_a, 3), **imbalance(trace.cpu().numpy(), c_np)}
+        res[name] = {"attn_ms": round(t_a, 3),
+                     **imbalance(trace.cpu().numpy(), c_np, tiling, fl == fva.FVA_SCHED_PERSISTENT)}
         log(f"[bench] stress {name}: {res[name]}")
     out["stress_scheduler"] = res
     del q, k, v, b, trace
@@ -736,7 +769,7 @@ def main():
             trace.zero_()
             attend(fl | fva.FVA_TRACE, trace)
             torch.cuda.synchronize()
-            imb[name] = imbalance(trace.cpu().numpy(), c_np)
+            imb[name] = imbalance(trace.cpu().numpy(), c_np, tiling, fl == fva.FVA_SCHED_PERSISTENT)
         res["scheduler_trace"] = imb
         log(f"[bench] trace: {imb}")
         # engine clock of the traced persistent run, and the attention's

@@ -58,3 +58,39 @@ def test_every_global_name_resolves():
 
     walk(top)
     assert not missing, sorted(missing)
+
+
+def _bench_module():
+    import importlib.util
+
+    spec = importlib.util.spec_from_file_location("bench_under_test", BENCH)
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_plan_costs_follow_the_pairing_rule():
+    import numpy as np
+
+    import paper_2607_16190_amd as fva
+
+    bench = _bench_module()
+    # 3 x 16 x 64 tokens in 1 x 8 x 8 boxes: 3 t-rows x 2 lines x 8 blocks,
+    # every block 64 tokens, so blocks (0,1), (2,3), ... pair; the automatic
+    # chunk size is 32 here, so row 5 (40 kept blocks) is split and its pair
+    # is not formed
+    t = fva.Tiling(3, 16, 64, 1, 8, 8)
+    c = np.full((1, 48), 3)
+    c[0, 0] = 7
+    c[0, 5] = 40
+    want = [4, 1] * 24
+    want[0] = 8
+    want[4], want[5] = 4, 41
+    assert [int(x) for x in bench.plan_costs(c, t, paired=True)] == want
+    assert [int(x) for x in bench.plan_costs(c, t, paired=False)] == list(c[0] + 1)
+    # 720p boxes: only the 60 blocks of the one-frame last t-row pair (5 per line)
+    t720 = fva.Tiling(21, 45, 80, 2, 8, 8)
+    c720 = np.full((1, 660), 10)
+    cost = bench.plan_costs(c720, t720, paired=True)
+    assert (cost == 1).sum() == 30 and (cost == 11).sum() == 630
+    assert list(np.nonzero(cost == 1)[0][:3]) == [601, 603, 605]
