@@ -209,12 +209,12 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "c61ab54109991c05",
+    "source_digest": "596f3a0249b3f5da",
     "bytes": {
-        "720p": ((111079208 + 112869768) // 2 * 2 + 758161) * 1024,
-        "720p-hilbert": ((77530191 + 78035132) // 2 * 2 + 758323) * 1024,
-        "720p-fp8v": ((70731104 + 70544653) // 2 * 2 + 758578) * 1024,
-        "720p-hilbert-fp8v": ((66796168 + 66587147) // 2 * 2 + 758506) * 1024,
+        "720p": ((114816830 + 116174200) // 2 * 2 + 758188) * 1024,
+        "720p-hilbert": ((78387704 + 78292995) // 2 * 2 + 758364) * 1024,
+        "720p-fp8v": ((70614626 + 70193745) // 2 * 2 + 758588) * 1024,
+        "720p-hilbert-fp8v": ((68412684 + 68461915) // 2 * 2 + 758504) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
@@ -222,10 +222,10 @@ ATTN_TRAFFIC = {
 ROUTE_TRAFFIC = {
     "source_digest": "892b2b78073cf628",
     "bytes": {
-        "720p": ((756174 + 29199 + 71521) * 2 + 53760 + 142494 + 49285) * 1024,
-        "720p-hilbert": ((756151 + 25338 + 58266) * 2 + 47360 + 117253 + 39989) * 1024,
-        "720p-fp8v": ((756174 + 29254 + 71556) * 2 + 53760 + 142399 + 49292) * 1024,
-        "720p-hilbert-fp8v": ((756150 + 25385 + 58256) * 2 + 47360 + 117109 + 39989) * 1024,
+        "720p": ((756174 + 29235 + 71545) * 2 + 53760 + 142379 + 49285) * 1024,
+        "720p-hilbert": ((756150 + 25335 + 58262) * 2 + 47360 + 117484 + 39989) * 1024,
+        "720p-fp8v": ((756174 + 29231 + 71576) * 2 + 53760 + 142386 + 49285) * 1024,
+        "720p-hilbert-fp8v": ((756150 + 25359 + 58250) * 2 + 47360 + 117112 + 39989) * 1024,
     },
 }
 

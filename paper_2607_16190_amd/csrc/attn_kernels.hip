@@ -110,7 +110,8 @@ struct BlockMap {
   int plane, ex;  // ey*ex and ex
   int mp, mx;     // ceil(2^16 / plane), ceil(2^16 / ex): exact quotients for rows < 128
   int n;          // real tokens
-  int pad0, pad1;
+  int pslot;      // query-block pair this block starts (slot within a head), or -1
+  int psecond;    // 1 when the block is the second of a pair
 };
 static_assert(sizeof(BlockMap) == 32, "one scalar load per record");
 
@@ -123,8 +124,8 @@ __device__ __forceinline__ BlockMap block_map(const Geometry& g, int j) {
   m.mp = (65536 + m.plane - 1) / m.plane;
   m.mx = (65536 + m.ex - 1) / m.ex;
   m.n = b.n;
-  m.pad0 = 0;
-  m.pad1 = 0;
+  m.pslot = pair_slot(g, j);
+  m.psecond = (j > 0 && pair_slot(g, j - 1) >= 0) ? 1 : 0;
   return m;
 }
 
@@ -139,8 +140,8 @@ __device__ __forceinline__ BlockMap load_block_map(const BlockMap* table, int j)
   m.mp = t[3];
   m.mx = t[4];
   m.n = t[5];
-  m.pad0 = 0;
-  m.pad1 = 0;
+  m.pslot = -1;  // (the block loop reads no pair fields)
+  m.psecond = 0;
   return m;
 }
 
@@ -929,12 +930,13 @@ constexpr int kQueues = 8;
 // 1 when it starts a pair (its item runs rows r and r + 1), 2 when it is the
 // second row of a pair (its item does nothing), 0 otherwise. A pair is formed
 // only when neither row is split (kept count <= S). The plan, the pair-list
-// kernel and the persistent kernel all decide it with this function.
-__device__ __forceinline__ int pair_role(const Geometry& g, const int32_t* __restrict__ counts, int r, int S) {
-  const int i = r % g.nb;
-  auto whole = [&](int rr) { return min(max(counts[rr], 0), g.nb) <= S; };
-  if (pair_slot(g, i) >= 0) return (whole(r) && whole(r + 1)) ? 1 : 0;
-  if (i > 0 && pair_slot(g, i - 1) >= 0) return (whole(r - 1) && whole(r)) ? 2 : 0;
+// kernel and the persistent kernel all decide it with this function, from
+// the block records' pair fields.
+__device__ __forceinline__ int pair_role(const BlockMap* __restrict__ table, const int32_t* __restrict__ counts,
+                                         int r, int i, int S, int nb) {
+  auto whole = [&](int rr) { return min(max(counts[rr], 0), nb) <= S; };
+  if (table[i].pslot >= 0) return (whole(r) && whole(r + 1)) ? 1 : 0;
+  if (table[i].psecond) return (whole(r - 1) && whole(r)) ? 2 : 0;
   return 0;
 }
 
@@ -989,11 +991,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
     float* partial = nullptr;
     int64_t rec = item;
     if (item >= 0) {
-      const int role = P.plist ? pair_role(P.g, P.counts, item, *P.psplit) : 0;
-      if (role == 1) {
-        const int bh = item / P.g.nb;
-        pslot = bh * P.pairs_head + pair_slot(P.g, item - bh * P.g.nb);
-      }
+      const int bh = item / P.g.nb;
+      const int i = item - bh * P.g.nb;
+      const int role = P.plist ? pair_role(P.bmap, P.counts, item, i, *P.psplit, P.g.nb) : 0;
+      if (role == 1) pslot = bh * P.pairs_head + P.bmap[i].pslot;
       rec = role == 2 ? -1 : item;  // the pair's item records the second row
     } else {
       const int c = -1 - item;
@@ -1050,11 +1051,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
                                                    int32_t* __restrict__ qbase, int32_t* __restrict__ qctr,
                                                    int32_t* __restrict__ hscratch, int32_t* __restrict__ rscratch,
                                                    int4* __restrict__ chunks, int4* __restrict__ splits,
-                                                   int32_t* __restrict__ n_split, int pairing,
-                                                   int32_t* __restrict__ psplit) {
+                                                   int32_t* __restrict__ n_split, const BlockMap* __restrict__ table,
+                                                   int pairing, int32_t* __restrict__ psplit) {
   __shared__ long long wtot[16];
   __shared__ int lds_order[kPlanLdsHeads];
   __shared__ int lds_len[kPlanLdsHeads * kQueues];
+  __shared__ unsigned char pcode[kMaxBlocks];
   const int nb = g.nb;
   const int rows = n_heads * nb;
   int32_t* hcost = hscratch;
@@ -1135,17 +1137,34 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   // items before row r (ipre[r])
   auto ipre = [&](int r) { return may_split ? r + cpre[r] - spre[r] : r; };
   if (pairing && threadIdx.x == 0) *psplit = S;
+  // Pair position of every block (1: first of a pair, 2: second, 0: none),
+  // from the block records once; the same rule as pair_role.
+  for (int i = threadIdx.x; i < nb; i += blockDim.x)
+    pcode[i] = !pairing ? 0 : (table[i].pslot >= 0 ? 1 : (table[i].psecond ? 2 : 0));
+  __syncthreads();
   auto cost_of = [&](int h, int i) {
     const int r = h * nb + i;
-    const int role = pairing ? pair_role(g, counts, r, S) : 0;
-    if (role == 1) return max(kept_of(r), kept_of(r + 1)) + 1;
-    return role == 2 ? 1 : kept_of(r) + 1;
+    const int code = pcode[i];
+    // the neighbours' counts load with the row's own (no dependent load)
+    const int c = kept_of(r);
+    const int cprev = i > 0 ? kept_of(r - 1) : 0;
+    const int cnext = i + 1 < nb ? kept_of(r + 1) : 0;
+    const int cn = code == 1 ? cnext : cprev;
+    if (code == 0 || c > S || cn > S) return c + 1;  // not in a formed pair
+    return code == 1 ? max(c, cn) + 1 : 1;
   };
 
-  // 2. head costs and equal-cost runs (one wave per head)
+  // 2. head costs and equal-cost runs (one wave per head); a lane's costs
+  //    stay in registers between the two passes
   for (int h = wave; h < n_heads; h += nwaves) {
+    int cst[kMaxBlocks / 64];
     int hsum = 0;
-    for (int i0 = 0; i0 < nb; i0 += 64) hsum += (i0 + lane < nb) ? cost_of(h, i0 + lane) : 0;
+#pragma unroll
+    for (int k = 0; k < kMaxBlocks / 64; ++k) {
+      const int i = 64 * k + lane;
+      cst[k] = i < nb ? cost_of(h, i) : 0;
+      hsum += cst[k];
+    }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) hsum += __shfl_xor(hsum, o);
     if (lane == 0) hcost[h] = hsum;
@@ -1156,9 +1175,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
 #pragma unroll
     for (int x = 0; x <= kQueues; ++x) stx[x] = nb;
     int run_before = 0;
-    for (int i0 = 0; i0 < nb; i0 += 64) {
+#pragma unroll
+    for (int k = 0; k < kMaxBlocks / 64; ++k) {
+      const int i0 = 64 * k;
+      if (i0 >= nb) break;
       const int i = i0 + lane;
-      const int c = i < nb ? cost_of(h, i) : 0;
+      const int c = cst[k];
       const int incl = wave_incl_scan_i32(c, lane);
       const int before = run_before + incl - c;
       const int run = (int)(((int64_t)before * kQueues) / hsum);
@@ -1265,27 +1287,29 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   if (threadIdx.x < kQueues) qctr[threadIdx.x] = 0;
 }
 
-// Union lists of the query-block pairs, one wave per row (rows that do not
-// start a pair leave at once): the two rows' kept sets become bitmaps in LDS,
+// Union lists of the query-block pairs, one wave per pair slot (pairs with a
+// split row are not formed and skipped): the two rows' kept sets become bitmaps in LDS,
 // read back in ascending block order as entries j | (j not kept by the first
 // row) << 16 | (j not kept by the second row) << 17. An entry repeated in a
 // kept list counts once.
 constexpr int kPairWords = kMaxBlocks / 64;
 
 __global__ __launch_bounds__(256) void pair_list_kernel(const int32_t* __restrict__ counts,
-                                                        const int32_t* __restrict__ kv_idx, int rows, Geometry g,
-                                                        int pairs_head, const int32_t* __restrict__ psplit,
-                                                        int32_t* __restrict__ plist, int32_t* __restrict__ pcount) {
+                                                        const int32_t* __restrict__ kv_idx, int n_heads, int nb,
+                                                        int pairs_head, const int32_t* __restrict__ pfirst,
+                                                        const int32_t* __restrict__ psplit, int32_t* __restrict__ plist,
+                                                        int32_t* __restrict__ pcount) {
   __shared__ unsigned long long bits[4][2 * kPairWords];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int nb = g.nb;
   const int S = *psplit;
+  const int n_pairs = n_heads * pairs_head;
   unsigned long long* bw = bits[wave];
-  for (int r = blockIdx.x * 4 + wave; r < rows; r += gridDim.x * 4) {
-    if (pair_role(g, counts, r, S) != 1) continue;
-    const int bh = r / nb;
-    const int slot = bh * pairs_head + pair_slot(g, r - bh * nb);
+  auto whole = [&](int rr) { return min(max(counts[rr], 0), nb) <= S; };
+  for (int slot = blockIdx.x * 4 + wave; slot < n_pairs; slot += gridDim.x * 4) {
+    const int bh = slot / pairs_head;
+    const int r = bh * nb + pfirst[slot - bh * pairs_head];
+    if (!whole(r) || !whole(r + 1)) continue;  // not formed: both rows run alone
     if (lane < 2 * kPairWords) bw[lane] = 0ull;
     wave_sync();
     for (int s = 0; s < 2; ++s) {
@@ -1309,7 +1333,7 @@ __global__ __launch_bounds__(256) void pair_list_kernel(const int32_t* __restric
       n += __popcll(m);
     }
     if (lane == 0) pcount[slot] = n;
-    wave_sync();  // the bitmaps are cleared for the next row only after every lane read them
+    wave_sync();  // the bitmaps are cleared for the next pair only after every lane read them
   }
 }
 
@@ -1357,9 +1381,15 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnParams P, const int4* 
 }
 
 // Block records of every block of the tiling (one thread per block).
-__global__ __launch_bounds__(256) void block_table_kernel(Geometry g, BlockMap* __restrict__ table) {
+// Block records, and (pfirst != null) the first block of every pair slot.
+__global__ __launch_bounds__(256) void block_table_kernel(Geometry g, BlockMap* __restrict__ table,
+                                                         int32_t* __restrict__ pfirst) {
   const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j < g.nb) table[j] = block_map(g, j);
+  if (j < g.nb) {
+    const BlockMap m = block_map(g, j);
+    table[j] = m;
+    if (pfirst && m.pslot >= 0) pfirst[m.pslot] = j;
+  }
 }
 
 // counts and ascending kept-block lists from a block mask, one wave per row.
@@ -1433,6 +1463,7 @@ struct AttnWorkspace {
   BlockMap* bmap;    // [nb]
   int32_t* plist;    // [pairs][nb]   union lists of query-block pairs (null: no pairing)
   int32_t* pcount;   // [pairs]
+  int32_t* pfirst;   // [pairs per head] first block of each pair slot
   int32_t* psplit;   // [1]           the plan's chunk size
   int pairs_head;    // pairs per head
   int cap;           // chunk records
@@ -1497,12 +1528,14 @@ AttnWorkspace carve(void* base, int batch, int heads, const Geometry& g, uint32_
   off += al((size_t)nb * sizeof(BlockMap));
   w.pairs_head = pairs_of(g, flags, lean);
   const size_t pairs = nh * (size_t)w.pairs_head;
-  w.plist = w.pcount = w.psplit = nullptr;
+  w.plist = w.pcount = w.pfirst = w.psplit = nullptr;
   if (pairs > 0) {
     w.plist = reinterpret_cast<int32_t*>(p + off);
     off += al(pairs * nb * 4);
     w.pcount = reinterpret_cast<int32_t*>(p + off);
     off += al(pairs * 4);
+    w.pfirst = reinterpret_cast<int32_t*>(p + off);
+    off += al((size_t)w.pairs_head * 4);
     w.psplit = reinterpret_cast<int32_t*>(p + off);
     off += al(4);
   }
@@ -1605,7 +1638,7 @@ hipError_t launch_attn(const AttnArgs& a) {
   P.psplit = ws.psplit;
   P.pairs_head = ws.pairs_head;
 
-  hipLaunchKernelGGL(block_table_kernel, dim3((g.nb + 255) / 256), dim3(256), 0, a.stream, g, ws.bmap);
+  hipLaunchKernelGGL(block_table_kernel, dim3((g.nb + 255) / 256), dim3(256), 0, a.stream, g, ws.bmap, ws.pfirst);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
 
@@ -1619,13 +1652,14 @@ hipError_t launch_attn(const AttnArgs& a) {
   const int forced = (int)((a.flags >> 8) & 0xFFFFu);
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, a.stream, counts, a.batch * a.heads, g, kSplitSlots, forced,
                      ws.cap, ws.items, ws.qbase, ws.qctr, ws.hscratch, ws.rscratch, ws.chunks, ws.splits, ws.n_split,
-                     ws.plist ? 1 : 0, ws.psplit);
+                     ws.bmap, ws.plist ? 1 : 0, ws.psplit);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (ws.plist) {
-    const int pgrid = std::max(1, std::min((n_items + 3) / 4, 4 * info.cus));
-    hipLaunchKernelGGL(pair_list_kernel, dim3(pgrid), dim3(256), 0, a.stream, counts, kv_idx, n_items, g,
-                       ws.pairs_head, ws.psplit, ws.plist, ws.pcount);
+    const int n_pairs = a.batch * a.heads * ws.pairs_head;
+    const int pgrid = std::max(1, std::min((n_pairs + 3) / 4, 4 * info.cus));
+    hipLaunchKernelGGL(pair_list_kernel, dim3(pgrid), dim3(256), 0, a.stream, counts, kv_idx, a.batch * a.heads,
+                       g.nb, ws.pairs_head, ws.pfirst, ws.psplit, ws.plist, ws.pcount);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

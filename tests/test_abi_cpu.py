@@ -64,12 +64,13 @@ def test_workspace_sizes():
         # counts, kept lists, queue items (rows + chunks), 9 queue bases, 8 queue
         # counters, per-head plan scratch, per-row prefixes, split count, chunk and
         # split records, partial results, one 32-byte record per block, then the
-        # query-block pairs' union lists, their lengths and the plan's chunk size
+        # query-block pairs' union lists, their lengths, the first block of each
+        # pair of a head and the plan's chunk size
         ws = (al(rows * 4) + al(rows * nb * 4) + al((rows + cap) * 4) + al(9 * 4) + al(8 * 4)
               + al(heads * 19 * 4) + al(2 * (rows + 1) * 4) + al(4) + 2 * al(cap * 16) + al(cap * part)
               + al(nb * 32))
         if pairs:
-            ws += al(pairs * nb * 4) + al(pairs * 4) + al(4)
+            ws += al(pairs * nb * 4) + al(pairs * 4) + al(pairs // heads * 4) + al(4)
         return ws
 
     # 720p: the 60 blocks of the last (one-frame) t-row hold 64 or 40 tokens,
@@ -117,7 +118,7 @@ def test_pair_count_matches_definition(grid, tile, expect):
     al = lambda x: (x + 255) // 256 * 256
     extra = fva.fva_attn_workspace_size(d, t) - fva.fva_attn_workspace_size(d, t, fva.FVA_SCHED_UNPAIRED)
     P = heads * want
-    assert extra == ((al(P * nb * 4) + al(P * 4) + al(4)) if P else 0)
+    assert extra == ((al(P * nb * 4) + al(P * 4) + al(want * 4) + al(4)) if P else 0)
 
 
 @pytest.mark.parametrize(
