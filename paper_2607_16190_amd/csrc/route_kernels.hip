@@ -212,6 +212,10 @@ __device__ __forceinline__ uint64_t block_mass(double s, double smax, double zs)
 constexpr uint64_t kOneCount = 1ull << 53;
 constexpr uint64_t kWeightBits = kOneCount - 1;
 
+// Largest candidate set the exact ranking of select_cut takes without one
+// more bucket level first.
+constexpr int kRankMax = 8;
+
 struct WaveScratch {
   uint64_t hist[64];  // packed bucket words
   double cs[64];      // candidates: score, weight, block id
@@ -286,9 +290,48 @@ __device__ Cut select_cut(const double (&s)[KPL], const uint64_t (&F)[KPL], uint
         c.rank = C0 + (int)t;
         return c;
       }
-      // At most 64 candidates, one per lane: each sums the weights of the
-      // candidates ahead of it (read as LDS broadcasts), so the crossing is
-      // the one candidate with before < thr <= before + own weight.
+      // More than kRankMax candidates of distinct scores: one more bucket
+      // level over them, one per lane (the rule of the levels below), so that
+      // the exact ranking that follows runs over the few of the crossing
+      // bucket. Compaction in lane order keeps ascending block ids.
+      if (ncand > kRankMax) {
+        const bool has0 = lane < ncand;
+        const double s0 = has0 ? ws.cs[lane] : 0.0;
+        const int j0 = has0 ? ws.cj[lane] : 0;
+        const uint64_t w0 = has0 ? ws.cw[lane] : 0ull;
+        const double lo0 = wave_min(has0 ? s0 : 1.0e308);
+        const double hi0 = wave_max(has0 ? s0 : -1.0e308);
+        if (hi0 > lo0) {
+          ws.hist[lane] = 0ull;
+          wave_sync();
+          int b = (int)__dmul_rn(hi0 - s0, 64.0 / (hi0 - lo0));
+          b = b < 0 ? 0 : (b > 63 ? 63 : b);
+          atomicAdd((unsigned long long*)&ws.hist[has0 ? b : lane],
+                    (unsigned long long)(has0 ? kOneCount + w0 : 0ull));
+          wave_sync();
+          const uint64_t hv = ws.hist[lane];
+          const uint64_t inc = wave_incl_scan_u64(hv, lane);
+          const uint64_t hit = __ballot(W0 + (inc & kWeightBits) >= thr);
+          const int bstar = hit ? (__ffsll((unsigned long long)hit) - 1) : 63;
+          const uint64_t ahead = lane_u64(inc - hv, bstar);
+          W0 += ahead & kWeightBits;
+          C0 += (int)(ahead >> 53);
+          const bool keep = has0 && b == bstar;
+          const uint64_t km = __ballot(keep);
+          ncand = __popcll(km);
+          if (keep) {
+            const int pos = lanes_below(km);
+            ws.cs[pos] = s0;
+            ws.cj[pos] = j0;
+            ws.cw[pos] = w0;
+          }
+          wave_sync();
+        }
+      }
+      // At most kRankMax candidates (or several of one score), one per lane:
+      // each sums the weights of the candidates ahead of it (read as LDS
+      // broadcasts), so the crossing is the one candidate with before < thr
+      // <= before + own weight.
       const bool has = lane < ncand;
       const double sl = has ? ws.cs[lane] : 0.0;
       const int jl = has ? ws.cj[lane] : 0;
