@@ -211,21 +211,21 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 ATTN_TRAFFIC = {
     "source_digest": "596f3a0249b3f5da",
     "bytes": {
-        "720p": ((114816830 + 116174200) // 2 * 2 + 758188) * 1024,
-        "720p-hilbert": ((78387704 + 78292995) // 2 * 2 + 758364) * 1024,
-        "720p-fp8v": ((70614626 + 70193745) // 2 * 2 + 758588) * 1024,
-        "720p-hilbert-fp8v": ((68412684 + 68461915) // 2 * 2 + 758504) * 1024,
+        "720p": ((115161258 + 115740057) // 2 * 2 + 758212) * 1024,
+        "720p-hilbert": ((78481659 + 79007616) // 2 * 2 + 758267) * 1024,
+        "720p-fp8v": ((70116825 + 70600499) // 2 * 2 + 758588) * 1024,
+        "720p-hilbert-fp8v": ((68453344 + 68580270) // 2 * 2 + 758487) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "892b2b78073cf628",
+    "source_digest": "db639e1075491557",
     "bytes": {
-        "720p": ((756174 + 29235 + 71545) * 2 + 53760 + 142379 + 49285) * 1024,
-        "720p-hilbert": ((756150 + 25335 + 58262) * 2 + 47360 + 117484 + 39989) * 1024,
-        "720p-fp8v": ((756174 + 29231 + 71576) * 2 + 53760 + 142386 + 49285) * 1024,
-        "720p-hilbert-fp8v": ((756150 + 25359 + 58250) * 2 + 47360 + 117112 + 39989) * 1024,
+        "720p": ((756174 + 29362 + 71590) * 2 + 53760 + 142548 + 49285) * 1024,
+        "720p-hilbert": ((756152 + 25326 + 58309) * 2 + 47360 + 117144 + 39989) * 1024,
+        "720p-fp8v": ((756174 + 29296 + 71644) * 2 + 53760 + 142432 + 49285) * 1024,
+        "720p-hilbert-fp8v": ((756152 + 25407 + 58310) * 2 + 47360 + 117470 + 39989) * 1024,
     },
 }
 
