@@ -82,26 +82,47 @@ def source_digest(*paths):
     return h.hexdigest()[:16]
 
 
+def pair_offsets(sizes, nby, nbx):
+    """Partner offset of every block (the library's pairing rule, restated):
+    x-neighbours (ix even, ix + 1) of one (t, y) line that both hold at most
+    64 tokens, then among the blocks no x-pair holds, y-neighbours (iy even,
+    iy + 1) of one (t, x) column that both do; +offset on the first block,
+    -offset on the second, 0 for blocks in no pair."""
+    n = sizes.reshape(-1, nby, nbx)
+    small = n <= 64
+    off = np.zeros(n.shape, np.int64)
+    inx = np.zeros(n.shape, bool)
+    for ix in range(0, nbx - 1, 2):
+        both = small[:, :, ix] & small[:, :, ix + 1]
+        off[:, :, ix] = np.where(both, 1, off[:, :, ix])
+        off[:, :, ix + 1] = np.where(both, -1, off[:, :, ix + 1])
+        inx[:, :, ix] |= both
+        inx[:, :, ix + 1] |= both
+    for iy in range(0, nby - 1, 2):
+        both = small[:, iy, :] & small[:, iy + 1, :] & ~inx[:, iy, :] & ~inx[:, iy + 1, :]
+        off[:, iy, :] = np.where(both, nbx, off[:, iy, :])
+        off[:, iy + 1, :] = np.where(both, -nbx, off[:, iy + 1, :])
+    return off.reshape(-1)
+
+
 def plan_costs(counts, tiling, paired):
     """Per-row cost the persistent plan balances: kept blocks + 1, except that
-    a query-block pair (x-neighbours ix even / ix + 1 of one (t, y) line, both
-    with at most 64 tokens, neither split) costs its larger row + 1 on its
-    first row and 1 on its second (the library's pairing rule, restated)."""
+    a query-block pair (pair_offsets; neither row split) costs its larger row
+    + 1 on its first row and 1 on its second."""
     c = np.clip(counts.reshape(-1, counts.shape[-1]).astype(np.int64), 0, counts.shape[-1])
     cost = c + 1
     if not paired:
         return cost.reshape(-1)
+    nby = -(-tiling.H // tiling.bh)
     nbx = -(-tiling.W // tiling.bw)
-    n = block_sizes((tiling.T, tiling.H, tiling.W), (tiling.bt, tiling.bh, tiling.bw)).reshape(-1, nbx)
-    n = n.reshape(-1, -(-tiling.H // tiling.bh), nbx)
-    first = np.zeros(n.shape, bool)
-    first[:, :, 0:nbx - 1:2] = (n[:, :, 0:nbx - 1:2] <= 64) & (n[:, :, 1::2] <= 64)
-    first = np.nonzero(first.reshape(-1))[0]
+    off = pair_offsets(block_sizes((tiling.T, tiling.H, tiling.W), (tiling.bt, tiling.bh, tiling.bw)), nby, nbx)
+    first = np.nonzero(off > 0)[0]
+    second = first + off[first]
     S = max(32, -(-int((c + 1).sum()) // 1024))  # the automatic chunk size
-    a, b = c[:, first], c[:, first + 1]
+    a, b = c[:, first], c[:, second]
     formed = (a <= S) & (b <= S)
     cost[:, first] = np.where(formed, np.maximum(a, b) + 1, cost[:, first])
-    cost[:, first + 1] = np.where(formed, 1, cost[:, first + 1])
+    cost[:, second] = np.where(formed, 1, cost[:, second])
     return cost.reshape(-1)
 
 

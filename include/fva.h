@@ -84,13 +84,15 @@ typedef struct fva_qkv_desc {
 #define FVA_SCHED_NAIVE 1u      /* one workgroup per item in head-major order (same kernel body) */
 #define FVA_TRACE 2u            /* record per-item start/end clock and CU id into `trace` */
 /* Persistent scheduler only: run every query block as an item of its own.
- * Without it, two x-neighbouring query blocks (ix, ix + 1), ix even, of one
- * (t, y) line that both hold at most 64 real tokens and are both unsplit run
- * as one 128-row item over the union of their kept lists (each block on two
- * of the four waves, each wave skipping the key blocks its block does not
- * keep), so that every K/V tile either keeps is staged once. Each row still
- * sees exactly its own key blocks in ascending order: the output is the
- * same bit for bit. */
+ * Without it, two neighbouring query blocks that both hold at most 64 real
+ * tokens and are both unsplit run as one 128-row item over the union of
+ * their kept lists (each block on two of the four waves, each wave skipping
+ * the key blocks its block does not keep), so that every K/V tile either
+ * keeps is staged once. Neighbours are x-neighbours (ix, ix + 1), ix even,
+ * of one (t, y) line; among the blocks no such pair holds, y-neighbours
+ * (iy, iy + 1), iy even, of one (t, x) column. Each row still sees exactly
+ * its own key blocks in ascending order: the output is the same bit for
+ * bit. */
 #define FVA_SCHED_UNPAIRED 4u
 /* Persistent scheduler only: split every row keeping more than s blocks into
  * ceil(count / s) chunk items of at most s blocks (1 <= s <= 65535). Without

@@ -23,12 +23,13 @@
 // launches the same item body once per item in head-major order.
 //
 // Query-block pairs: blocks of at most 64 real tokens (partial boxes at the
-// end of the t or y axis, or every block of a 64-token tiling) fill only two
-// of the four waves, and a CU's other workgroup cannot use the idle SIMDs
-// because its own waves move in step through their barriers. Two such
-// x-neighbours run as one item instead: each on two waves, over the union of
-// their kept lists (neighbouring blocks keep nearly the same key blocks), so
-// every SIMD works and each K/V tile is staged once for both.
+// end of an axis, or every block of a 64-token tiling) fill only two of the
+// four waves, and a CU's other workgroup cannot use the idle SIMDs because
+// its own waves move in step through their barriers. Two such neighbours
+// (x-neighbours, else y-neighbours) run as one item instead: each on two
+// waves, over the union of their kept lists (neighbouring blocks keep nearly
+// the same key blocks), so every SIMD works and each K/V tile is staged once
+// for both.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -111,7 +112,7 @@ struct BlockMap {
   int mp, mx;     // ceil(2^16 / plane), ceil(2^16 / ex): exact quotients for rows < 128
   int n;          // real tokens
   int pslot;      // query-block pair this block starts (slot within a head), or -1
-  int psecond;    // 1 when the block is the second of a pair
+  int poff;       // block-id offset of its pair partner (> 0: it starts the pair), 0: none
 };
 static_assert(sizeof(BlockMap) == 32, "one scalar load per record");
 
@@ -124,8 +125,8 @@ __device__ __forceinline__ BlockMap block_map(const Geometry& g, int j) {
   m.mp = (65536 + m.plane - 1) / m.plane;
   m.mx = (65536 + m.ex - 1) / m.ex;
   m.n = b.n;
-  m.pslot = pair_slot(g, j);
-  m.psecond = (j > 0 && pair_slot(g, j - 1) >= 0) ? 1 : 0;
+  m.pslot = -1;  // numbered by block_table_kernel
+  m.poff = pair_partner(g, j);
   return m;
 }
 
@@ -141,7 +142,7 @@ __device__ __forceinline__ BlockMap load_block_map(const BlockMap* table, int j)
   m.mx = t[4];
   m.n = t[5];
   m.pslot = -1;  // (the block loop reads no pair fields)
-  m.psecond = 0;
+  m.poff = 0;
   return m;
 }
 
@@ -306,8 +307,8 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // kept-list entries [begin, end) of its row. partial == nullptr: the whole
 // row, normalised into O; otherwise one chunk of a split row, whose
 // unnormalised result goes to partial for the combine step. pslot >= 0: the
-// query-block pair (i, i + 1) of that slot, block i on waves 0-1 and block
-// i + 1 on waves 2-3, over the union of their kept lists; a wave skips the
+// query-block pair (i, i2) of that slot, block i on waves 0-1 and block i2
+// on waves 2-3, over the union of their kept lists; a wave skips the
 // key blocks its own block does not keep, so each row sees exactly its own
 // blocks in ascending order, as when the two run alone.
 //
@@ -317,7 +318,8 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // tile), the scales entering as the MFMA's E8M0 block scales.
 template <bool F8>
 __device__ void process_item(const AttnParams& P, int row, int begin, int end, float* __restrict__ partial,
-                             unsigned char* __restrict__ Ks, unsigned char* __restrict__ Vs, int pslot = -1) {
+                             unsigned char* __restrict__ Ks, unsigned char* __restrict__ Vs, int pslot = -1,
+                             int i2 = 0) {
   const int nb = P.g.nb;
   const int bh = row / nb;
   const int i = row - bh * nb;
@@ -335,7 +337,7 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
   const bool paired = pslot >= 0;
   const int half = paired ? wave >> 1 : 0;  // which block of a pair
   const int hbit = paired ? 1 << half : 0;  // this wave's skip bit in a pair's entries
-  const BlockBox bi = block_box(P.g, i + half);
+  const BlockBox bi = block_box(P.g, half ? i2 : i);
   const int row0 = paired ? 32 * (wave & 1) : 32 * wave;
   const bool active = row0 < bi.n;
 
@@ -882,21 +884,22 @@ __device__ void process_item(const AttnParams& P, int row, int begin, int end, f
 // shader-clock cycles (s_memtime) it took, so that the engine clock of the
 // run is the ratio of the two clocks. A pair's item fills the records of
 // both its rows, splitting its time evenly between them. One thread writes.
-__device__ __forceinline__ void trace_record(const AttnParams& P, int64_t rec, bool pair, int64_t t0, int64_t t1,
+__device__ __forceinline__ void trace_record(const AttnParams& P, int64_t rec, int poff, int64_t t0, int64_t t1,
                                              int64_t cycles) {
   const int64_t loc = (int64_t)hw_location();
   int64_t* tr = P.trace + rec * 4;
-  if (pair) {
+  if (poff) {  // a pair: the second row's record is poff records on
     const int64_t tm = t0 + (t1 - t0) / 2;
     const int64_t cm = cycles / 2;
+    int64_t* t2 = tr + 4 * (int64_t)poff;
     tr[0] = t0;
     tr[1] = tm;
     tr[2] = loc;
     tr[3] = cm;
-    tr[4] = tm;
-    tr[5] = t1;
-    tr[6] = loc;
-    tr[7] = cycles - cm;
+    t2[0] = tm;
+    t2[1] = t1;
+    t2[2] = loc;
+    t2[3] = cycles - cm;
   } else {
     tr[0] = t0;
     tr[1] = t1;
@@ -916,7 +919,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams 
     __syncthreads();
     if (threadIdx.x == 0) {
       const int64_t c1 = (int64_t)__builtin_amdgcn_s_memtime();
-      trace_record(P, blockIdx.x, false, t0, (int64_t)wall_clock64(), c1 - c0);
+      trace_record(P, blockIdx.x, 0, t0, (int64_t)wall_clock64(), c1 - c0);
     }
   }
 }
@@ -935,9 +938,9 @@ constexpr int kQueues = 8;
 __device__ __forceinline__ int pair_role(const BlockMap* __restrict__ table, const int32_t* __restrict__ counts,
                                          int r, int i, int S, int nb) {
   auto whole = [&](int rr) { return min(max(counts[rr], 0), nb) <= S; };
-  if (table[i].pslot >= 0) return (whole(r) && whole(r + 1)) ? 1 : 0;
-  if (table[i].psecond) return (whole(r - 1) && whole(r)) ? 2 : 0;
-  return 0;
+  const int poff = table[i].poff;
+  if (poff == 0 || !whole(r) || !whole(r + poff)) return 0;
+  return poff > 0 ? 1 : 2;
 }
 
 __device__ __forceinline__ int xcc_id() {
@@ -959,10 +962,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
   // region that only thread 0 runs, so the compiler keeps every lane of
   // every wave on one path through the loop and its barriers.
   int64_t prec = -1, pt0 = 0, pt1 = 0, pcyc = 0;
-  bool ppair = false;
+  int ppoff = 0;
   for (;;) {
     if (threadIdx.x == 0) {
-      if (prec >= 0) trace_record(P, prec, ppair, pt0, pt1, pcyc);
+      if (prec >= 0) trace_record(P, prec, ppoff, pt0, pt1, pcyc);
       int slot = -1, qq = q;
       for (int t = 0; t < kQueues; ++t) {
         qq = (q + t) % kQueues;
@@ -987,14 +990,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
     const int64_t c0 = P.trace ? (int64_t)__builtin_amdgcn_s_memtime() : 0;
     // One call site for every kind of item (rows, pairs, chunks), so that the
     // item body is inlined once.
-    int row = item, begin = 0, end = P.g.nb, pslot = -1;
+    int row = item, begin = 0, end = P.g.nb, pslot = -1, poff = 0, i2 = 0;
     float* partial = nullptr;
     int64_t rec = item;
     if (item >= 0) {
       const int bh = item / P.g.nb;
       const int i = item - bh * P.g.nb;
       const int role = P.plist ? pair_role(P.bmap, P.counts, item, i, *P.psplit, P.g.nb) : 0;
-      if (role == 1) pslot = bh * P.pairs_head + P.bmap[i].pslot;
+      if (role == 1) {
+        pslot = bh * P.pairs_head + P.bmap[i].pslot;
+        poff = P.bmap[i].poff;
+        i2 = i + poff;
+      }
       rec = role == 2 ? -1 : item;  // the pair's item records the second row
     } else {
       const int c = -1 - item;
@@ -1006,11 +1013,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_persistent_kernel(AttnPa
       partial = P.partials + (int64_t)c * kPartialFloats;
       rec = c < P.trace_chunks ? P.n_rows + c : -2;
     }
-    if (rec != -1) process_item<F8>(P, row, begin, end, partial, ks_tile, vs_tile, pslot);
+    if (rec != -1) process_item<F8>(P, row, begin, end, partial, ks_tile, vs_tile, pslot, i2);
     __syncthreads();  // the next item's copies overwrite the tiles; next_slot is rewritten
     if (P.trace) {
       prec = rec;
-      ppair = pslot >= 0;
+      ppoff = poff;
       pt0 = t0;
       pt1 = (int64_t)wall_clock64();
       pcyc = (int64_t)__builtin_amdgcn_s_memtime() - c0;
@@ -1056,7 +1063,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   __shared__ long long wtot[16];
   __shared__ int lds_order[kPlanLdsHeads];
   __shared__ int lds_len[kPlanLdsHeads * kQueues];
-  __shared__ unsigned char pcode[kMaxBlocks];
+  __shared__ int poffs[kMaxBlocks];
   const int nb = g.nb;
   const int rows = n_heads * nb;
   int32_t* hcost = hscratch;
@@ -1137,21 +1144,17 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   // items before row r (ipre[r])
   auto ipre = [&](int r) { return may_split ? r + cpre[r] - spre[r] : r; };
   if (pairing && threadIdx.x == 0) *psplit = S;
-  // Pair position of every block (1: first of a pair, 2: second, 0: none),
-  // from the block records once; the same rule as pair_role.
-  for (int i = threadIdx.x; i < nb; i += blockDim.x)
-    pcode[i] = !pairing ? 0 : (table[i].pslot >= 0 ? 1 : (table[i].psecond ? 2 : 0));
+  // Pair partner offset of every block (> 0: first of a pair, < 0: second,
+  // 0: none), from the block records once; the same rule as pair_role.
+  for (int i = threadIdx.x; i < nb; i += blockDim.x) poffs[i] = pairing ? table[i].poff : 0;
   __syncthreads();
   auto cost_of = [&](int h, int i) {
     const int r = h * nb + i;
-    const int code = pcode[i];
-    // the neighbours' counts load with the row's own (no dependent load)
+    const int poff = poffs[i];
     const int c = kept_of(r);
-    const int cprev = i > 0 ? kept_of(r - 1) : 0;
-    const int cnext = i + 1 < nb ? kept_of(r + 1) : 0;
-    const int cn = code == 1 ? cnext : cprev;
-    if (code == 0 || c > S || cn > S) return c + 1;  // not in a formed pair
-    return code == 1 ? max(c, cn) + 1 : 1;
+    const int cn = poff ? kept_of(r + poff) : 0;
+    if (poff == 0 || c > S || cn > S) return c + 1;  // not in a formed pair
+    return poff > 0 ? max(c, cn) + 1 : 1;
   };
 
   // 2. head costs and equal-cost runs (one wave per head); a lane's costs
@@ -1296,7 +1299,8 @@ constexpr int kPairWords = kMaxBlocks / 64;
 
 __global__ __launch_bounds__(256) void pair_list_kernel(const int32_t* __restrict__ counts,
                                                         const int32_t* __restrict__ kv_idx, int n_heads, int nb,
-                                                        int pairs_head, const int32_t* __restrict__ pfirst,
+                                                        const BlockMap* __restrict__ table, int pairs_head,
+                                                        const int32_t* __restrict__ pfirst,
                                                         const int32_t* __restrict__ psplit, int32_t* __restrict__ plist,
                                                         int32_t* __restrict__ pcount) {
   __shared__ unsigned long long bits[4][2 * kPairWords];
@@ -1308,13 +1312,16 @@ __global__ __launch_bounds__(256) void pair_list_kernel(const int32_t* __restric
   auto whole = [&](int rr) { return min(max(counts[rr], 0), nb) <= S; };
   for (int slot = blockIdx.x * 4 + wave; slot < n_pairs; slot += gridDim.x * 4) {
     const int bh = slot / pairs_head;
-    const int r = bh * nb + pfirst[slot - bh * pairs_head];
-    if (!whole(r) || !whole(r + 1)) continue;  // not formed: both rows run alone
+    const int i = pfirst[slot - bh * pairs_head];
+    const int r = bh * nb + i;
+    const int r2 = r + table[i].poff;
+    if (!whole(r) || !whole(r2)) continue;  // not formed: both rows run alone
     if (lane < 2 * kPairWords) bw[lane] = 0ull;
     wave_sync();
     for (int s = 0; s < 2; ++s) {
-      const int c = min(max(counts[r + s], 0), nb);
-      const int32_t* kv = kv_idx + (int64_t)(r + s) * nb;
+      const int rs = s ? r2 : r;
+      const int c = min(max(counts[rs], 0), nb);
+      const int32_t* kv = kv_idx + (int64_t)rs * nb;
       for (int a = lane; a < c; a += 64) {
         const int j = min(max(kv[a], 0), nb - 1);
         atomicOr(&bw[s * kPairWords + (j >> 6)], 1ull << (j & 63));
@@ -1380,15 +1387,32 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnParams P, const int4* 
   }
 }
 
-// Block records of every block of the tiling (one thread per block).
-// Block records, and (pfirst != null) the first block of every pair slot.
-__global__ __launch_bounds__(256) void block_table_kernel(Geometry g, BlockMap* __restrict__ table,
-                                                         int32_t* __restrict__ pfirst) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
+static_assert(kMaxBlocks <= 1024, "block_table_kernel runs one thread per block in one workgroup");
+
+// Block records of every block of the tiling, one thread per block in one
+// workgroup (nb <= 1024), the query-block pairs numbered in the order of
+// their first block; and (pfirst != null) the first block of every pair.
+__global__ __launch_bounds__(1024) void block_table_kernel(Geometry g, BlockMap* __restrict__ table,
+                                                          int32_t* __restrict__ pfirst) {
+  __shared__ int wsum[1024 / 64];
+  const int j = threadIdx.x;
+  const int lane = j & 63;
+  const int wave = j >> 6;
+  BlockMap m = {};
+  int first = 0;
   if (j < g.nb) {
-    const BlockMap m = block_map(g, j);
+    m = block_map(g, j);
+    first = m.poff > 0 ? 1 : 0;
+  }
+  const int incl = wave_incl_scan_i32(first, lane);
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int before = incl - first;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  if (j < g.nb) {
+    m.pslot = first ? before : -1;
     table[j] = m;
-    if (pfirst && m.pslot >= 0) pfirst[m.pslot] = j;
+    if (pfirst && first) pfirst[before] = j;
   }
 }
 
@@ -1638,7 +1662,7 @@ hipError_t launch_attn(const AttnArgs& a) {
   P.psplit = ws.psplit;
   P.pairs_head = ws.pairs_head;
 
-  hipLaunchKernelGGL(block_table_kernel, dim3((g.nb + 255) / 256), dim3(256), 0, a.stream, g, ws.bmap, ws.pfirst);
+  hipLaunchKernelGGL(block_table_kernel, dim3(1), dim3(1024), 0, a.stream, g, ws.bmap, ws.pfirst);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
 
@@ -1659,7 +1683,7 @@ hipError_t launch_attn(const AttnArgs& a) {
     const int n_pairs = a.batch * a.heads * ws.pairs_head;
     const int pgrid = std::max(1, std::min((n_pairs + 3) / 4, 4 * info.cus));
     hipLaunchKernelGGL(pair_list_kernel, dim3(pgrid), dim3(256), 0, a.stream, counts, kv_idx, a.batch * a.heads,
-                       g.nb, ws.pairs_head, ws.pfirst, ws.psplit, ws.plist, ws.pcount);
+                       g.nb, ws.bmap, ws.pairs_head, ws.pfirst, ws.psplit, ws.plist, ws.pcount);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -53,40 +53,51 @@ __host__ __device__ inline BlockBox block_box(const Geometry& g, int i) {
   return b;
 }
 
-// Query-block pairs. Two x-neighbouring blocks (ix, ix + 1), ix even, of the
-// same (t, y) line are one pair when both hold at most 64 real tokens; the
-// attention then runs them as one 128-row work item (each block on two
-// waves) that stages every key block kept by either once. Block ix is not the
-// last of its line, so its x extent is bw and block ix + 1 is no larger: a
-// line pairs all its floor(nbx / 2) pairs or none, decided by et * ey * bw.
-__host__ __device__ inline bool line_pairs(const Geometry& g, int et, int ey) { return et * ey * g.bw <= 64; }
-
-// Lines of t-row it (extent et) that pair.
-__host__ __device__ inline int paired_lines_of_row(const Geometry& g, int et) {
-  const int ey_last = g.H - (g.nby - 1) * g.bh;
-  return (g.nby - 1) * (line_pairs(g, et, g.bh) ? 1 : 0) + (line_pairs(g, et, ey_last) ? 1 : 0);
+// Query-block pairs: two neighbouring blocks that both hold at most 64 real
+// tokens, run by the attention as one 128-row work item (each block on two
+// waves) that stages every key block kept by either once.
+//  * x-pairs: (ix, ix + 1), ix even, of one (t, y) line. Block ix is not the
+//    last of its line, so its x extent is bw and block ix + 1 is no larger:
+//    a line pairs all its floor(nbx / 2) pairs or none (et * ey * bw <= 64).
+//  * y-pairs, among the blocks no x-pair holds (the lines that do not pair,
+//    and the last block of a pairing line when nbx is odd): (iy, iy + 1),
+//    iy even, of one (t, x) column, both holding at most 64 tokens.
+// pair_partner(g, i) is the block-id offset of i's partner: +1 or +nbx when
+// i starts a pair, -1 or -nbx when it is the second block, 0 otherwise.
+// Pairs are numbered per head in the order of their first block.
+__host__ __device__ inline int block_tokens(const Geometry& g, int it, int iy, int ix) {
+  return min(g.bt, g.T - it * g.bt) * min(g.bh, g.H - iy * g.bh) * min(g.bw, g.W - ix * g.bw);
 }
 
-// Pairs in one head (every head has the same).
-__host__ __device__ inline int pairs_per_head(const Geometry& g) {
-  const int et_last = g.T - (g.nbt - 1) * g.bt;
-  const int lines = (g.nbt - 1) * paired_lines_of_row(g, g.bt) + paired_lines_of_row(g, et_last);
-  return lines * (g.nbx / 2);
+// Block (it, iy, ix) belongs to an x-pair.
+__host__ __device__ inline bool in_x_pair(const Geometry& g, int it, int iy, int ix) {
+  const int et = min(g.bt, g.T - it * g.bt);
+  const int ey = min(g.bh, g.H - iy * g.bh);
+  return et * ey * g.bw <= 64 && ix < 2 * (g.nbx / 2);
 }
 
-// Slot of the pair whose first block is i within its head (pairs numbered in
-// raster order of their first block), or -1 when i does not start a pair.
-__host__ __device__ inline int pair_slot(const Geometry& g, int i) {
+// y-pair (iy, iy + 1) starting at (it, iy, ix), iy even.
+__host__ __device__ inline bool y_pair_at(const Geometry& g, int it, int iy, int ix) {
+  return iy + 1 < g.nby && !in_x_pair(g, it, iy, ix) && !in_x_pair(g, it, iy + 1, ix) &&
+         block_tokens(g, it, iy, ix) <= 64 && block_tokens(g, it, iy + 1, ix) <= 64;
+}
+
+__host__ __device__ inline int pair_partner(const Geometry& g, int i) {
   const int it = i / (g.nby * g.nbx);
   const int rem = i - it * (g.nby * g.nbx);
   const int iy = rem / g.nbx;
   const int ix = rem - iy * g.nbx;
-  const int et = min(g.bt, g.T - it * g.bt);
-  const int ey = min(g.bh, g.H - iy * g.bh);
-  if ((ix & 1) || ix + 1 >= g.nbx || !line_pairs(g, et, ey)) return -1;
-  // t-rows before it are full in t, lines before iy in this row full in y
-  const int lines_before = it * paired_lines_of_row(g, g.bt) + iy * (line_pairs(g, et, g.bh) ? 1 : 0);
-  return lines_before * (g.nbx / 2) + ix / 2;
+  if (in_x_pair(g, it, iy, ix)) return (ix & 1) ? -1 : 1;
+  if (!(iy & 1) && y_pair_at(g, it, iy, ix)) return g.nbx;
+  if ((iy & 1) && y_pair_at(g, it, iy - 1, ix)) return -g.nbx;
+  return 0;
+}
+
+// Pairs in one head (every head has the same).
+__host__ __device__ inline int pairs_per_head(const Geometry& g) {
+  int n = 0;
+  for (int i = 0; i < g.nb; ++i) n += pair_partner(g, i) > 0 ? 1 : 0;
+  return n;
 }
 
 // Global token index of the r-th real token (local raster order) of a box.

@@ -12,6 +12,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_2607_16190_amd as fva
@@ -85,12 +86,27 @@ def test_workspace_sizes():
 
 def _pairs_by_definition(T, H, W, bt, bh, bw):
     """Query-block pairs of one head, counted block by block: x-neighbours
-    (ix, ix + 1) with ix even of one (t, y) line, both holding <= 64 tokens."""
+    (ix even, ix + 1) of one (t, y) line, both holding <= 64 tokens; then,
+    among the blocks no x-pair holds, y-neighbours (iy even, iy + 1) of one
+    (t, x) column, both holding <= 64 tokens."""
     from oracle import tile_geometry
 
     geo = tile_geometry(T, H, W, bt, bh, bw)
     n = geo.block_sizes.reshape(geo.nbt, geo.nby, geo.nbx)
-    return int(((n[:, :, 0:geo.nbx - 1:2] <= 64) & (n[:, :, 1::2] <= 64)).sum())
+    taken = np.zeros(n.shape, bool)
+    count = 0
+    for t in range(geo.nbt):
+        for y in range(geo.nby):
+            for x in range(0, geo.nbx - 1, 2):
+                if n[t, y, x] <= 64 and n[t, y, x + 1] <= 64:
+                    taken[t, y, x] = taken[t, y, x + 1] = True
+                    count += 1
+    for t in range(geo.nbt):
+        for x in range(geo.nbx):
+            for y in range(0, geo.nby - 1, 2):
+                if not taken[t, y, x] and not taken[t, y + 1, x] and n[t, y, x] <= 64 and n[t, y + 1, x] <= 64:
+                    count += 1
+    return count
 
 
 @pytest.mark.parametrize(
@@ -98,7 +114,7 @@ def _pairs_by_definition(T, H, W, bt, bh, bw):
     [
         ((21, 45, 80), (2, 8, 8), 30),      # 720p: the one-frame last t-row
         ((31, 45, 80), (2, 8, 8), 30),      # long clip
-        ((21, 30, 52), (2, 8, 8), None),    # 480p: partial boxes on all three axes
+        ((21, 30, 52), (2, 8, 8), 34),      # 480p: 12 x-pairs, 22 y-pairs of the 4-token-wide column
         ((3, 16, 16), (1, 8, 8), 6),        # 64-token boxes: every line pairs
         ((5, 17, 23), (1, 8, 8), None),     # odd block counts per line
         ((9, 20, 40), (2, 4, 8), None),     # 64-token boxes of another shape

@@ -88,6 +88,17 @@ def test_plan_costs_follow_the_pairing_rule():
     want[4], want[5] = 4, 41
     assert [int(x) for x in bench.plan_costs(c, t, paired=True)] == want
     assert [int(x) for x in bench.plan_costs(c, t, paired=False)] == list(c[0] + 1)
+    # 480p boxes (21 x 30 x 52 in 2 x 8 x 8, 11 x 4 x 7 blocks): the
+    # one-frame last t-row x-pairs (3 per line), and the last, 4-token-wide
+    # column pairs along y in every t-row (2 per column): 12 + 22 pairs
+    t480 = fva.Tiling(21, 30, 52, 2, 8, 8)
+    off = bench.pair_offsets(bench.block_sizes((21, 30, 52), (2, 8, 8)), 4, 7)
+    assert (off == 1).sum() == 12 and (off == 7).sum() == 22 and (off > 0).sum() == 34
+    assert off[6] == 7 and off[13] == -7 and off[20] == 7 and off[27] == -7  # column ix = 6, t-row 0
+    assert off[280] == 1 and off[281] == -1 and off[286] == 7  # last t-row: x-pairs, then its column
+    c480 = np.full((1, 308), 10)
+    cost = bench.plan_costs(c480, t480, paired=True)
+    assert (cost == 1).sum() == 34 and cost[6] == 11 and cost[13] == 1
     # 720p boxes: only the 60 blocks of the one-frame last t-row pair (5 per line)
     t720 = fva.Tiling(21, 45, 80, 2, 8, 8)
     c720 = np.full((1, 660), 10)

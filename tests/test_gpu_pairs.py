@@ -1,13 +1,15 @@
 """Query-block pairs of the persistent scheduler.
 
-Two x-neighbouring query blocks of at most 64 real tokens run as one item
-over the union of their kept lists, each on two of the four waves, each wave
+Two neighbouring query blocks of at most 64 real tokens (x-neighbours, else
+y-neighbours) run as one item over the union of their kept lists, each on
+two of the four waves, each wave
 skipping the key blocks its own block does not keep. Every row therefore
 sees exactly its own key blocks in ascending order, as it does alone: the
 paired launch must equal, bit for bit, the same launch under
 FVA_SCHED_UNPAIRED and the naive grid, on every kind of workload that forms
-pairs (one-frame last t-rows, partial boxes on every axis, 64-token boxes,
-64-token curve runs, split rows next to paired ones, E4M3 V). The oracle
+pairs (one-frame last t-rows, the narrow last column of 480p, partial boxes
+on every axis, 64-token boxes, 64-token curve runs, split rows next to
+paired ones, E4M3 V). The oracle
 parity of the same launches is covered by the other attention tests, which
 run the default (paired) path.
 """
@@ -23,16 +25,26 @@ pytestmark = pytest.mark.gpu
 
 
 def pairs_of(geo):
-    """(first block, second block) of every pair of one head, by definition."""
+    """(first block, second block) of every pair of one head, by definition:
+    x-neighbours (ix even, ix + 1) of one (t, y) line with at most 64 tokens
+    each; then, among the blocks no x-pair holds, y-neighbours (iy even,
+    iy + 1) of one (t, x) column with at most 64 tokens each."""
     n = geo.block_sizes.reshape(geo.nbt, geo.nby, geo.nbx)
-    out = []
+    bid = lambda t, y, x: (t * geo.nby + y) * geo.nbx + x
+    out, taken = [], set()
     for t in range(geo.nbt):
         for y in range(geo.nby):
             for x in range(0, geo.nbx - 1, 2):
                 if n[t, y, x] <= 64 and n[t, y, x + 1] <= 64:
-                    i = (t * geo.nby + y) * geo.nbx + x
-                    out.append((i, i + 1))
-    return out
+                    out.append((bid(t, y, x), bid(t, y, x + 1)))
+                    taken |= {bid(t, y, x), bid(t, y, x + 1)}
+    for t in range(geo.nbt):
+        for x in range(geo.nbx):
+            for y in range(0, geo.nby - 1, 2):
+                a, b = bid(t, y, x), bid(t, y + 1, x)
+                if a not in taken and b not in taken and n[t, y, x] <= 64 and n[t, y + 1, x] <= 64:
+                    out.append((a, b))
+    return sorted(out)
 
 
 def split_rows(mask_np):
@@ -91,14 +103,15 @@ def test_pairs_equal_unpaired_on_routed_workloads(name, heads):
 @pytest.mark.parametrize("s", [2, 5])
 def test_pairs_next_to_split_rows(s):
     # Partial boxes on all three axes (5 = 2*2 + 1 frames, 13 = 8 + 5 rows,
-    # 21 = 2*8 + 5 columns): the one-frame t-row forms the pairs (12, 13) and
-    # (15, 16). Random masks elsewhere; in every head row 13 keeps s + 2
-    # blocks (split into chunks, so its pair is not formed) and rows 15 and
-    # 16 keep at most s blocks, one shared and one of their own each (paired).
+    # 21 = 2*8 + 5 columns): the one-frame t-row forms the x-pairs (12, 13)
+    # and (15, 16) and the y-pair (14, 17) of its narrow last column. Random
+    # masks elsewhere; in every head row 13 keeps s + 2 blocks (split into
+    # chunks, so its pair is not formed) and rows 15 and 16 keep at most s
+    # blocks, one shared and one of their own each (paired).
     fva, torch = lib(), torch_mod()
     cfg = custom_config("pairsplit", 3, (5, 13, 21), (2, 8, 8), (0.3, 1.5, 5.0), seed=41)
     geo = geometry_of(cfg)
-    assert pairs_of(geo) == [(12, 13), (15, 16)]
+    assert pairs_of(geo) == [(12, 13), (14, 17), (15, 16)]
     Qb, Kb, Vb = synth.gen_qkv(cfg)
     rng = np.random.default_rng(43 + s)
     m = (rng.random((1, 3, geo.nb, geo.nb)) < 0.25).astype(np.uint8)
