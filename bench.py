@@ -230,23 +230,23 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "596f3a0249b3f5da",
+    "source_digest": "1838d50025ccfd1d",
     "bytes": {
-        "720p": ((115161258 + 115740057) // 2 * 2 + 758212) * 1024,
-        "720p-hilbert": ((78481659 + 79007616) // 2 * 2 + 758267) * 1024,
-        "720p-fp8v": ((70116825 + 70600499) // 2 * 2 + 758588) * 1024,
-        "720p-hilbert-fp8v": ((68453344 + 68580270) // 2 * 2 + 758487) * 1024,
+        "720p": ((110331510 + 111929930) // 2 * 2 + 758232) * 1024,
+        "720p-hilbert": ((77098072 + 77594403) // 2 * 2 + 758270) * 1024,
+        "720p-fp8v": ((70717424 + 72080444) // 2 * 2 + 758585) * 1024,
+        "720p-hilbert-fp8v": ((67155941 + 67270230) // 2 * 2 + 758507) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "db639e1075491557",
+    "source_digest": "cb2069381ee48a84",
     "bytes": {
-        "720p": ((756174 + 29362 + 71590) * 2 + 53760 + 142548 + 49285) * 1024,
-        "720p-hilbert": ((756152 + 25326 + 58309) * 2 + 47360 + 117144 + 39989) * 1024,
-        "720p-fp8v": ((756174 + 29296 + 71644) * 2 + 53760 + 142432 + 49285) * 1024,
-        "720p-hilbert-fp8v": ((756152 + 25407 + 58310) * 2 + 47360 + 117470 + 39989) * 1024,
+        "720p": ((756174 + 29216 + 71579) * 2 + 53760 + 142557 + 49285) * 1024,
+        "720p-hilbert": ((756150 + 25287 + 58324) * 2 + 47360 + 117235 + 39989) * 1024,
+        "720p-fp8v": ((756174 + 29246 + 71642) * 2 + 53760 + 142769 + 49285) * 1024,
+        "720p-hilbert-fp8v": ((756150 + 25303 + 58277) * 2 + 47360 + 117282 + 39989) * 1024,
     },
 }
 
