@@ -930,11 +930,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_naive_kernel(AttnParams 
 constexpr int kQueues = 8;
 
 // Role of row r (= bh * nb + i) under query-block pairing with chunk size S:
-// 1 when it starts a pair (its item runs rows r and r + 1), 2 when it is the
-// second row of a pair (its item does nothing), 0 otherwise. A pair is formed
-// only when neither row is split (kept count <= S). The plan, the pair-list
-// kernel and the persistent kernel all decide it with this function, from
-// the block records' pair fields.
+// 1 when it starts a pair (its item runs row r and its partner's row), 2
+// when it is the second row of a pair (its item does nothing), 0 otherwise.
+// A pair is formed only when neither row is split (kept count <= S). The
+// persistent kernel decides it with this function, from the block records'
+// partner offsets; the plan and the pair-list kernel apply the same test.
 __device__ __forceinline__ int pair_role(const BlockMap* __restrict__ table, const int32_t* __restrict__ counts,
                                          int r, int i, int S, int nb) {
   auto whole = [&](int rr) { return min(max(counts[rr], 0), nb) <= S; };
