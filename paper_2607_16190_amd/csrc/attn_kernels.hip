@@ -1181,18 +1181,19 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
 #pragma unroll
     for (int k = 0; k < kMaxBlocks / 64; ++k) {
       const int i0 = 64 * k;
-      if (i0 >= nb) break;
-      const int i = i0 + lane;
-      const int c = cst[k];
-      const int incl = wave_incl_scan_i32(c, lane);
-      const int before = run_before + incl - c;
-      const int run = (int)(((int64_t)before * kQueues) / hsum);
+      if (i0 < nb) {  // (a guard, not a break: the loop stays unrolled and cst in registers)
+        const int i = i0 + lane;
+        const int c = cst[k];
+        const int incl = wave_incl_scan_i32(c, lane);
+        const int before = run_before + incl - c;
+        const int run = (int)(((int64_t)before * kQueues) / hsum);
 #pragma unroll
-      for (int x = 0; x < kQueues; ++x) {
-        const uint64_t hit = __ballot(i < nb && run >= x);
-        if (stx[x] == nb && hit) stx[x] = i0 + __ffsll((unsigned long long)hit) - 1;
+        for (int x = 0; x < kQueues; ++x) {
+          const uint64_t hit = __ballot(i < nb && run >= x);
+          if (stx[x] == nb && hit) stx[x] = i0 + __ffsll((unsigned long long)hit) - 1;
+        }
+        run_before += __shfl(incl, 63);
       }
-      run_before += __shfl(incl, 63);
     }
     int32_t* st = hstart + (size_t)h * (kQueues + 1);
     if (lane == 0) {
