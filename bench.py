@@ -230,12 +230,12 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "1838d50025ccfd1d",
+    "source_digest": "3ef400a2539b49b9",
     "bytes": {
-        "720p": ((110331510 + 111929930) // 2 * 2 + 758232) * 1024,
-        "720p-hilbert": ((77098072 + 77594403) // 2 * 2 + 758270) * 1024,
-        "720p-fp8v": ((70717424 + 72080444) // 2 * 2 + 758585) * 1024,
-        "720p-hilbert-fp8v": ((67155941 + 67270230) // 2 * 2 + 758507) * 1024,
+        "720p": ((111061526 + 111029686) // 2 * 2 + 758184) * 1024,
+        "720p-hilbert": ((77461667 + 76782158) // 2 * 2 + 758301) * 1024,
+        "720p-fp8v": ((71406886 + 71808663) // 2 * 2 + 758600) * 1024,
+        "720p-hilbert-fp8v": ((67137811 + 66650041) // 2 * 2 + 758482) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
@@ -243,10 +243,10 @@ ATTN_TRAFFIC = {
 ROUTE_TRAFFIC = {
     "source_digest": "cb2069381ee48a84",
     "bytes": {
-        "720p": ((756174 + 29216 + 71579) * 2 + 53760 + 142557 + 49285) * 1024,
-        "720p-hilbert": ((756150 + 25287 + 58324) * 2 + 47360 + 117235 + 39989) * 1024,
-        "720p-fp8v": ((756174 + 29246 + 71642) * 2 + 53760 + 142769 + 49285) * 1024,
-        "720p-hilbert-fp8v": ((756150 + 25303 + 58277) * 2 + 47360 + 117282 + 39989) * 1024,
+        "720p": ((756174 + 29237 + 71572) * 2 + 53760 + 142645 + 49285) * 1024,
+        "720p-hilbert": ((756151 + 25332 + 58287) * 2 + 47360 + 117248 + 39989) * 1024,
+        "720p-fp8v": ((756174 + 29250 + 71638) * 2 + 53760 + 142411 + 49285) * 1024,
+        "720p-hilbert-fp8v": ((756149 + 25311 + 58328) * 2 + 47360 + 117435 + 39989) * 1024,
     },
 }
 
