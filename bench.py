@@ -252,11 +252,14 @@ ROUTE_TRAFFIC = {
 
 
 def extra_workloads(torch, fva, synth, dev, reps=3):
-    """The other two timed workloads, outside the timed region, as extra keys.
+    """The other timed workloads, outside the timed region, as extra keys.
 
     long: the 31x45x80 clip (111,600 tokens, nb 960) at p = 0.8, 0.9 and 0.95:
     retained fraction, route and attention times (HIP events, mean of reps
     after one warmup each).
+    480p: the 21x30x52 clip (32,760 tokens, nb 308, partial boxes on all
+    three axes) at p = 0.9: the same figures plus the useful (real token
+    pair) rate.
     720p_stress: 8 flat and 32 concentrated heads of the 720p shape: attention
     time under the persistent scheduler and under the naive head-major grid,
     and from one traced run of each the per-CU busy max/mean, the per-XCD
@@ -320,6 +323,29 @@ def extra_workloads(torch, fva, synth, dev, reps=3):
         log(f"[bench] long p={pp}: {sweep[-1]}")
     out["long_p_sweep"] = {"workload": f"long: {q.shape[1]} heads, 31x45x80 = {cfg.N} tokens, tile 2x8x8, nb={nb}, "
                                        f"k_min={cfg.k_min}", "reps": reps, "points": sweep}
+    del q, k, v, b
+    torch.cuda.empty_cache()
+
+    # 480p: most of its blocks are partial boxes (query-block pairs along x
+    # and y)
+    cfg, tiling, nb, (q, k, v), b = load("480p")
+    route_fn = lambda: fva.fva_route(q, k, cfg.p, cfg.k_min, tiling, out=(b["mask"], b["counts"], b["kv"]),
+                                     workspace=b["ws_r"])
+    attn_fn = lambda: fva.fva_attn(q, k, v, tiling, b["mask"], b["counts"], b["kv"], out=b["out"],
+                                   workspace=b["ws_a"])
+    t_r, t_a = timed_pair(route_fn, attn_fn)
+    m_np = b["mask"].cpu().numpy()
+    kept = int(m_np.sum())
+    useful = 4.0 * 128 * real_pairs(m_np, block_sizes(cfg.grid, cfg.tile))
+    dense = 4.0 * q.shape[1] * float(cfg.N) ** 2 * 128
+    out["p480"] = {"workload": f"480p: {q.shape[1]} heads, 21x30x52 = {cfg.N} tokens, tile 2x8x8, nb={nb}, "
+                               f"p={cfg.p}, k_min={cfg.k_min}", "reps": reps,
+                   "retained_fraction": round(kept / (q.shape[1] * nb * nb), 4),
+                   "route_us": round(t_r * 1e3, 1), "attn_ms": round(t_a, 3),
+                   "kept_tile_TFLOPS": round(4.0 * 128**3 * kept / (t_a / 1e3) / 1e12, 1),
+                   "useful_TFLOPS": round(useful / (t_a / 1e3) / 1e12, 1),
+                   "dense_equiv_TFLOPS": round(dense / ((t_r + t_a) / 1e3) / 1e12, 1)}
+    log(f"[bench] 480p: {out['p480']}")
     del q, k, v, b
     torch.cuda.empty_cache()
 
