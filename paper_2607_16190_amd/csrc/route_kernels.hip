@@ -442,17 +442,19 @@ __device__ __forceinline__ void select_row(const double* __restrict__ srow, int 
   uint64_t F[KPL];
   uint32_t valid = 0;
   double vmax = -1.0e308, vmin = 1.0e308;
+  // All KPL loads of a lane are issued before any is used (lanes past the
+  // row re-read its last score, so no load is conditional), so the row waits
+  // for one memory latency rather than KPL dependent ones. Each score row is
+  // read once here.
+#pragma unroll
+  for (int k = 0; k < KPL; ++k) s[k] = __builtin_nontemporal_load(srow + min(lane + 64 * k, nb - 1));
 #pragma unroll
   for (int k = 0; k < KPL; ++k) {
-    const int j = lane + 64 * k;
-    if (j < nb) {
-      s[k] = __builtin_nontemporal_load(srow + j);  // each score row is read once
-      valid |= 1u << k;
-      vmax = fmax(vmax, s[k]);
-      vmin = fmin(vmin, s[k]);
-    } else {
-      s[k] = -1.0e308;
-    }
+    const bool in = lane + 64 * k < nb;
+    valid |= in ? 1u << k : 0u;
+    s[k] = in ? s[k] : -1.0e308;
+    vmax = fmax(vmax, s[k]);
+    vmin = in ? fmin(vmin, s[k]) : vmin;
   }
   const double smax = wave_max(vmax);
   const double smin = wave_min(vmin);
@@ -669,30 +671,34 @@ __global__ __launch_bounds__(64 * kRowWaves, KPL > 12 ? 3 : 4) void augment_kern
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t row = (int64_t)blockIdx.x * kRowWaves + wave;
   if (row >= nrows) return;
+  // The head's extra count, the row's count and its cut do not depend on one
+  // another: loaded together, ahead of the test that needs the first two.
   const int e = __builtin_amdgcn_readfirstlane(extra[row / nb]);
-  if (e <= 0) return;
-  const int m0 = min(max(__builtin_amdgcn_readfirstlane(counts[row]), 0), nb);
-  if (m0 >= nb) return;
-  const double s_cut = cuts[row].s;
-  const int j_cut = __builtin_amdgcn_readfirstlane(cuts[row].j);
+  const int c0 = __builtin_amdgcn_readfirstlane(counts[row]);
+  const RowCut rc = cuts[row];
+  const double s_cut = rc.s;
+  const int j_cut = __builtin_amdgcn_readfirstlane(rc.j);
+  asm volatile("" ::"v"(s_cut), "s"(j_cut));
+  const int m0 = min(max(c0, 0), nb);
+  if ((e <= 0) | (m0 >= nb)) return;
   const double* srow = scores + row * nb;
   double s[KPL];
   uint64_t F[KPL];
   uint32_t cand = 0;
   double cmax = -1.0e308, cmin = 1.0e308;
+  // every load of the row in flight at once, as in select_row
+#pragma unroll
+  for (int k = 0; k < KPL; ++k) s[k] = srow[min(lane + 64 * k, nb - 1)];
 #pragma unroll
   for (int k = 0; k < KPL; ++k) {
     const int j = lane + 64 * k;
     F[k] = 0ull;
-    s[k] = -1.0e308;
-    if (j < nb) {
-      s[k] = srow[j];
-      if (s[k] < s_cut || (s[k] == s_cut && j > j_cut)) {
-        cand |= 1u << k;
-        cmax = fmax(cmax, s[k]);
-        cmin = fmin(cmin, s[k]);
-      }
-    }
+    const bool in = j < nb;
+    s[k] = in ? s[k] : -1.0e308;
+    const bool c = in && (s[k] < s_cut || (s[k] == s_cut && j > j_cut));
+    cand |= c ? 1u << k : 0u;
+    cmax = c ? fmax(cmax, s[k]) : cmax;
+    cmin = c ? fmin(cmin, s[k]) : cmin;
   }
   int ncand = 0;
 #pragma unroll
@@ -738,10 +744,16 @@ __global__ __launch_bounds__(1024) void sasa_budget_kernel(const int32_t* __rest
   }
   __syncthreads();
   for (int h = wave; h < n_heads; h += nwaves) {
+    // nb <= kMaxBlocks: a lane's counts of the head, all loads in flight at once
+    const int32_t* crow = counts + (int64_t)h * nb;
+    int c[kMaxBlocks / 64];
+#pragma unroll
+    for (int k = 0; k < kMaxBlocks / 64; ++k) c[k] = crow[min(lane + 64 * k, nb - 1)];
     unsigned long long sum = 0ull;
-    for (int i = lane; i < nb; i += 64) {
-      const int c = counts[(int64_t)h * nb + i];
-      sum += (unsigned long long)(c < 0 ? 0 : (c > nb ? nb : c));
+#pragma unroll
+    for (int k = 0; k < kMaxBlocks / 64; ++k) {
+      const int ck = c[k] < 0 ? 0 : (c[k] > nb ? nb : c[k]);
+      sum += lane + 64 * k < nb ? (unsigned long long)ck : 0ull;
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
