@@ -1062,10 +1062,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
                                                    int pairing, int32_t* __restrict__ psplit) {
   __shared__ long long wtot[16];
   __shared__ int lds_order[kPlanLdsHeads];
+  __shared__ int lds_cost[kPlanLdsHeads];
   __shared__ int lds_len[kPlanLdsHeads * kQueues];
   __shared__ int poffs[kMaxBlocks];
   const int nb = g.nb;
   const int rows = n_heads * nb;
+  const bool in_lds = n_heads <= kPlanLdsHeads;
   int32_t* hcost = hscratch;
   int32_t* horder = hcost + n_heads;
   int32_t* hstart = horder + n_heads;                  // [n_heads][kQueues + 1]
@@ -1080,9 +1082,20 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
     return c < 0 ? 0 : (c > nb ? nb : c);
   };
 
-  // 0. chunk size
+  // 0. chunk size. One workgroup does all of the plan, so its time is load
+  //    latency: every thread keeps eight loads in flight per step (lanes past
+  //    the last row re-read it), here and in the passes below.
   long long tsum = 0;
-  for (int r = threadIdx.x; r < rows; r += blockDim.x) tsum += kept_of(r) + 1;
+  for (int r0 = threadIdx.x; r0 < rows; r0 += 8 * (int)blockDim.x) {
+    int c8[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) c8[u] = counts[min((int64_t)r0 + (int64_t)u * blockDim.x, (int64_t)rows - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int c = c8[u] < 0 ? 0 : (c8[u] > nb ? nb : c8[u]);
+      tsum += (int64_t)r0 + (int64_t)u * blockDim.x < rows ? c + 1 : 0;
+    }
+  }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) tsum += __shfl_xor(tsum, o);
   if (lane == 0) wtot[wave] = tsum;
@@ -1148,29 +1161,42 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   // 0: none), from the block records once; the same rule as pair_role.
   for (int i = threadIdx.x; i < nb; i += blockDim.x) poffs[i] = pairing ? table[i].poff : 0;
   __syncthreads();
-  auto cost_of = [&](int h, int i) {
-    const int r = h * nb + i;
-    const int poff = poffs[i];
-    const int c = kept_of(r);
-    const int cn = poff ? kept_of(r + poff) : 0;
+  // cost of a row from its partner offset, its kept count and its partner's
+  auto row_cost = [&](int poff, int c, int cn) {
     if (poff == 0 || c > S || cn > S) return c + 1;  // not in a formed pair
     return poff > 0 ? max(c, cn) + 1 : 1;
   };
+  auto clamp_count = [&](int c) { return c < 0 ? 0 : (c > nb ? nb : c); };
 
-  // 2. head costs and equal-cost runs (one wave per head); a lane's costs
-  //    stay in registers between the two passes
+  // 2. head costs and equal-cost runs (one wave per head): every count the
+  //    head's costs need is loaded first (lanes past nb re-read the last
+  //    block's; an unpaired row reads its own count as its partner's); a
+  //    lane's costs stay in registers between the two passes
   for (int h = wave; h < n_heads; h += nwaves) {
+    const int32_t* hc = counts + (size_t)h * nb;
+    int pf[kMaxBlocks / 64], ca[kMaxBlocks / 64], cb[kMaxBlocks / 64];
+#pragma unroll
+    for (int k = 0; k < kMaxBlocks / 64; ++k) pf[k] = poffs[min(64 * k + lane, nb - 1)];
+#pragma unroll
+    for (int k = 0; k < kMaxBlocks / 64; ++k) {
+      const int i = min(64 * k + lane, nb - 1);
+      ca[k] = hc[i];
+      cb[k] = hc[i + pf[k]];
+    }
     int cst[kMaxBlocks / 64];
     int hsum = 0;
 #pragma unroll
     for (int k = 0; k < kMaxBlocks / 64; ++k) {
-      const int i = 64 * k + lane;
-      cst[k] = i < nb ? cost_of(h, i) : 0;
+      const int cost = row_cost(pf[k], clamp_count(ca[k]), clamp_count(cb[k]));
+      cst[k] = 64 * k + lane < nb ? cost : 0;
       hsum += cst[k];
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) hsum += __shfl_xor(hsum, o);
-    if (lane == 0) hcost[h] = hsum;
+    if (lane == 0) {
+      hcost[h] = hsum;
+      if (in_lds) lds_cost[h] = hsum;
+    }
     // run of row i = floor(kQueues * (cost before row i) / hsum), a
     // non-decreasing function of i; run x starts at the first row whose run
     // is >= x (nb when there is none).
@@ -1186,10 +1212,11 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
         const int c = cst[k];
         const int incl = wave_incl_scan_i32(c, lane);
         const int before = run_before + incl - c;
-        const int run = (int)(((int64_t)before * kQueues) / hsum);
+        // run >= x exactly when kQueues * before >= x * hsum: no division,
+        // and no overflow (before <= hsum <= nb * (nb + 1))
 #pragma unroll
         for (int x = 0; x < kQueues; ++x) {
-          const uint64_t hit = __ballot(i < nb && run >= x);
+          const uint64_t hit = __ballot(i < nb && before * kQueues >= x * hsum);
           if (stx[x] == nb && hit) stx[x] = i0 + __ffsll((unsigned long long)hit) - 1;
         }
         run_before += __shfl(incl, 63);
@@ -1203,29 +1230,36 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   }
   __syncthreads();
 
-  // 3. head order by decreasing cost (ties: lower head first)
-  for (int h = threadIdx.x; h < n_heads; h += blockDim.x) {
-    const int ch = hcost[h];
+  // 3. head order by decreasing cost (ties: lower head first), from the LDS
+  //    copy of the costs when it holds them
+  auto rank_by_cost = [&](const int32_t* costs, int h) {
+    const int ch = costs[h];
     int rank = 0;
     for (int k = 0; k < n_heads; ++k) {
-      const int ck = hcost[k];
+      const int ck = costs[k];
       rank += (ck > ch || (ck == ch && k < h)) ? 1 : 0;
     }
-    horder[rank] = h;
-  }
+    return rank;
+  };
+  for (int h = threadIdx.x; h < n_heads; h += blockDim.x)
+    horder[in_lds ? rank_by_cost(lds_cost, h) : rank_by_cost(hcost, h)] = h;
   __syncthreads();
 
   // 4. queue offsets (in items) of every (head, run) and queue bases: a
   //    walk over the heads in cost order, from LDS copies of the order and
   //    of the item count of every (head, run) when they fit
-  const bool in_lds = n_heads <= kPlanLdsHeads;
   if (in_lds) {
     for (int r = threadIdx.x; r < n_heads; r += blockDim.x) {
       const int h = horder[r];
       const int32_t* st = hstart + (size_t)h * (kQueues + 1);
+      int stx[kQueues + 1], ip[kQueues + 1];
+#pragma unroll
+      for (int x = 0; x <= kQueues; ++x) stx[x] = st[x];
+#pragma unroll
+      for (int x = 0; x <= kQueues; ++x) ip[x] = ipre(h * nb + stx[x]);
       lds_order[r] = h;
 #pragma unroll
-      for (int x = 0; x < kQueues; ++x) lds_len[r * kQueues + x] = ipre(h * nb + st[x + 1]) - ipre(h * nb + st[x]);
+      for (int x = 0; x < kQueues; ++x) lds_len[r * kQueues + x] = ip[x + 1] - ip[x];
     }
     __syncthreads();
   }
@@ -1263,12 +1297,16 @@ __global__ __launch_bounds__(1024) void plan_kernel(const int32_t* __restrict__ 
   //    records; one wave per head, whose run x fills one contiguous slice of
   //    queue x. Then reset the queue counters.
   for (int h = wave; h < n_heads; h += nwaves) {
+    // the head's run starts and the start of its slice of every queue, one
+    // per lane, loaded together
     const int32_t* st = hstart + (size_t)h * (kQueues + 1);
+    const int st_l = lane <= kQueues ? st[lane] : 0;
+    const int off_l = lane < kQueues ? qbase[lane] + hoff[(size_t)h * kQueues + lane] : 0;
     for (int x = 0; x < kQueues; ++x) {
-      const int i_begin = __builtin_amdgcn_readfirstlane(st[x]);
-      const int i_end = __builtin_amdgcn_readfirstlane(st[x + 1]);
+      const int i_begin = __builtin_amdgcn_readlane(st_l, x);
+      const int i_end = __builtin_amdgcn_readlane(st_l, x + 1);
       if (i_begin >= i_end) continue;
-      const int slice = qbase[x] + hoff[(size_t)h * kQueues + x] - ipre(h * nb + i_begin);
+      const int slice = __builtin_amdgcn_readlane(off_l, x) - ipre(h * nb + i_begin);
       for (int i = i_begin + lane; i < i_end; i += 64) {
         const int r = h * nb + i;
         const int pos = slice + ipre(r);
