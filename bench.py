@@ -230,23 +230,23 @@ def cpu_baseline(cfg, Qb, Kb, Vb, mask, counts, budget_s=20.0, blocks="box"):
 # counter reads for a device copy of known size; valid only for the attention
 # source with this digest (null otherwise).
 ATTN_TRAFFIC = {
-    "source_digest": "3ef400a2539b49b9",
+    "source_digest": "f8dc17fcc7ddf8c6",
     "bytes": {
-        "720p": ((111061526 + 111029686) // 2 * 2 + 758184) * 1024,
-        "720p-hilbert": ((77461667 + 76782158) // 2 * 2 + 758301) * 1024,
-        "720p-fp8v": ((71406886 + 71808663) // 2 * 2 + 758600) * 1024,
-        "720p-hilbert-fp8v": ((67137811 + 66650041) // 2 * 2 + 758482) * 1024,
+        "720p": ((111222344 + 111111162) // 2 * 2 + 758186) * 1024,
+        "720p-hilbert": ((77795484 + 77549784) // 2 * 2 + 758302) * 1024,
+        "720p-fp8v": ((71772201 + 70525558) // 2 * 2 + 758575) * 1024,
+        "720p-hilbert-fp8v": ((66644817 + 67124268) // 2 * 2 + 758497) * 1024,
     },
 }
 # Same for fva_route (pool_kernel + score_kernel + select_kernel), per call
 # (FETCH x 2, WRITE x 1, KiB per dispatch summed over the three kernels).
 ROUTE_TRAFFIC = {
-    "source_digest": "cb2069381ee48a84",
+    "source_digest": "d8fe57f482ee46fc",
     "bytes": {
-        "720p": ((756174 + 29237 + 71572) * 2 + 53760 + 142645 + 49285) * 1024,
-        "720p-hilbert": ((756151 + 25332 + 58287) * 2 + 47360 + 117248 + 39989) * 1024,
-        "720p-fp8v": ((756174 + 29250 + 71638) * 2 + 53760 + 142411 + 49285) * 1024,
-        "720p-hilbert-fp8v": ((756149 + 25311 + 58328) * 2 + 47360 + 117435 + 39989) * 1024,
+        "720p": ((756175 + 29245 + 68473) * 2 + 53760 + 142312 + 49285) * 1024,
+        "720p-hilbert": ((756151 + 25345 + 55227) * 2 + 47360 + 116782 + 39989) * 1024,
+        "720p-fp8v": ((756173 + 29198 + 68476) * 2 + 53760 + 142496 + 49285) * 1024,
+        "720p-hilbert-fp8v": ((756150 + 25344 + 55238) * 2 + 47360 + 116986 + 39989) * 1024,
     },
 }
 
