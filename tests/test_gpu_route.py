@@ -130,6 +130,27 @@ def test_route_deterministic():
     assert np.array_equal(k1[valid], k2[valid])  # entries past counts are unspecified
 
 
+# Block counts on both sides of every multiple of 64 that selects a
+# different number of scores per lane (1..16): a row's last lane group is
+# then full, holds one block, or (nb = 1) only lane 0 holds a block. One
+# line of 64-token blocks with a short last block, two heads (a flat and a
+# concentrated one).
+WAVE_EDGE_NB = [1, 63, 64, 65, 128, 129, 256, 257, 511, 513, 768, 769, 1024]
+
+
+def line_config(name, nb, seed, alphas=(0.5, 3.0)):
+    n = 40 if nb == 1 else 64 * nb - 17
+    return custom_config(name, len(alphas), (1, 1, n), (1, 1, 64), alphas, seed=seed)
+
+
+@pytest.mark.parametrize("nb", WAVE_EDGE_NB)
+def test_route_block_counts_at_wave_edges(nb):
+    cfg = line_config(f"edge{nb}", nb, seed=60 + nb % 37)
+    assert geometry_of(cfg).nb == nb
+    Qb, Kb, _ = synth.gen_qkv(cfg)
+    check_route(f"edge nb={nb}", Qb, Kb, cfg, cfg.p, cfg.k_min)
+
+
 def test_route_max_blocks():
     # nb = 1024, the largest supported block count: 16 x 128 x 64 tokens, 2x8x8 boxes.
     cfg = custom_config("max_blocks", 1, (16, 128, 64), (2, 8, 8), (1.5,), seed=11)

@@ -131,6 +131,17 @@ def test_sasa_batch_two():
     log(f"[sasa] batch 2: extra per rank {e_use.tolist()}")
 
 
+@pytest.mark.parametrize("nb", [1, 64, 65, 129, 257, 513, 769, 1024])
+def test_sasa_block_counts_at_wave_edges(nb):
+    # a line of 64-token blocks (short last block), a flat head on rank 0
+    # and a concentrated one on rank 1: rank 1 is augmented
+    n = 40 if nb == 1 else 64 * nb - 17
+    cfg = custom_config(f"sasa_edge{nb}", 2, (1, 1, n), (1, 1, 64), (0.5, 3.0), seed=90 + nb % 31)
+    assert geometry_of(cfg).nb == nb
+    Qb, Kb, _ = synth.gen_qkv(cfg)
+    check(f"edge nb={nb}", Qb, Kb, cfg, [0, 1], 2, n1=0.8, n2=0.0)
+
+
 def test_sasa_one_rank_per_head_and_max_ranks():
     cfg = synth.get_config("480p")
     Qb, Kb, _ = workload("480p")
