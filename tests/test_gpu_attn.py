@@ -239,6 +239,30 @@ def test_attn_batch_two_odd_heads():
     compare_full("batch2", Qb, Kb, Vb, cfg, mask.cpu().numpy(), o64(O_p))
 
 
+def test_attn_more_heads_than_plan_lds():
+    # 2 x 520 = 1040 (batch, head) pairs, more than the 1024 whose costs,
+    # order and queue lengths the plan keeps in LDS: it takes them from the
+    # workspace instead. The grid's one-frame last t-row forms query-block
+    # pairs. The persistent launch must equal the unpaired one and the naive
+    # grid bit for bit (no row is split: nb = 8), and a few heads the oracle.
+    fva, torch = lib(), torch_mod()
+    heads = 520
+    alphas = tuple(float(a) for a in np.random.default_rng(71).uniform(0.3, 5.0, heads))
+    cfg = synth.WorkloadConfig("manyheads", heads, (3, 16, 16), (2, 8, 8), 0.9, 2, 71, "fixed", alphas, batch=2)
+    assert cfg.batch * cfg.heads > 1024 and geometry_of(cfg).nb == 8
+    Qb, Kb, Vb = synth.gen_qkv(cfg)
+    q, k, v = upload(Qb, Kb, Vb)
+    mask, counts, kv = fva.fva_route(q, k, cfg.p, cfg.k_min, tiling_of(cfg))
+    O_p = run_attn(q, k, v, cfg, mask, counts, kv)
+    O_u = run_attn(q, k, v, cfg, mask, counts, kv, flags=fva.FVA_SCHED_UNPAIRED)
+    O_n = run_attn(q, k, v, cfg, mask, counts, kv, flags=fva.FVA_SCHED_NAIVE)
+    assert torch.equal(O_p, O_u) and torch.equal(O_p, O_n)
+    sel = [0, 137, 519]
+    m = mask.cpu().numpy()
+    O = o64(O_p)
+    compare_full("1040 heads, 2 x 3 of them", Qb[:, sel], Kb[:, sel], Vb[:, sel], cfg, m[:, sel], O[:, sel])
+
+
 @pytest.mark.parametrize("s", [1, 2, 3, 5])
 @pytest.mark.parametrize("grid,tile", [((3, 16, 16), (1, 8, 8)), ((5, 13, 21), (2, 8, 8))])
 def test_attn_split_forced(s, grid, tile):
