@@ -127,7 +127,10 @@ fva_status fva_route_workspace_size(const fva_qkv_desc* desc, const fva_tiling* 
  * as exact fixed-point masses (2^-52 quanta), so the decision c_r >= p agrees
  * with an fp64 sequential sum except within about 1e-6 of p.
  *
- * Inputs : Q, K (bf16, desc), p in [0, 1], k_min >= 0, tiling.
+ * Inputs : Q, K (bf16, desc), p in [0, 1], k_min >= 0, tiling. Q and K are
+ *          taken to be finite: with NaN or infinite elements the call still
+ *          writes every output in bounds and returns, but which blocks a
+ *          row keeps is unspecified.
  * Outputs: block_mask uint8 [batch, heads, nb, nb] (1 = kept), fully written;
  *          counts int32 [batch, heads, nb] = m per row, fully written;
  *          kv_idx int32 [batch, heads, nb, nb] or NULL: row (b,h,i) holds the
